@@ -1,0 +1,185 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) mixture-of-experts FFN block.
+ *
+ * The block is the expert layer of a Qwen3-30B-A3B-style MoE reranker: the
+ * paper (§3, Expert-Parallel MoE Training) routes each token to its top-8 of
+ * 128 experts and, under expert parallelism, dispatches routed tokens to the
+ * ranks that hold their experts (§3, "Expert parallelism and topology").  The
+ * operations below are, in order:
+ *
+ *   forward   z = x W_r (fp32 logits); per valid token the top-k experts
+ *             (descending logit, ties to the lower expert index) and gates
+ *             g = softmax over the k selected logits; a stable permutation of
+ *             the routed (token, slot) pairs into expert-major, token-ascending
+ *             rows; Xp[r] = x[row_token[r]]; per expert e on its rows
+ *             G = Xp W_gate[e], U = Xp W_up[e], A = silu(G) * U, O = A W_down[e];
+ *             Y[t] = sum_j g[t,j] O[row_of[t,j]].
+ *   backward  dO = g dY and dg = <dY, O> per routed row; dA = dO W_down^T;
+ *             dG = dA U s (1 + G (1 - s)), dU = dA silu(G) with s = sigmoid(G);
+ *             dXp = dG W_gate^T + dU W_up^T; dW_down = A^T dO,
+ *             dW_gate = Xp^T dG, dW_up = Xp^T dU per expert (zero for experts
+ *             with no rows); dz = g (dg - sum_j g dg) on the selected experts;
+ *             dW_r = x^T dz; dX[t] = sum_j dXp[row_of[t,j]] + dz[t] W_r^T.
+ *
+ * The paper does not print these equations; the readings taken where it is
+ * silent (selection precision, tie-break, gate placement, padding, dropless
+ * routing, no auxiliary loss) are the ones stated above.
+ *
+ * Conventions shared by every entry point
+ *   - All tensors are row-major and live in device memory owned by the
+ *     caller; the library never allocates or frees device memory.
+ *   - "bf16" tensors are IEEE bfloat16 (2 bytes); accumulation is fp32.
+ *   - Every device pointer must be 16-byte aligned.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream) and never synchronise the host; counts stay on the device.
+ *   - All argument checks happen before any launch: on an error nothing is
+ *     launched and an MOE_ERR_* code is returned; moe_last_error() then
+ *     describes it (thread-local string, valid until the next call on the
+ *     same thread).
+ *   - Results are deterministic: two calls with the same inputs produce the
+ *     same bits (no atomics decide any floating-point summation order).
+ *   - No thread safety is promised for concurrent calls sharing buffers.
+ */
+#ifndef MOE_MI355X_H
+#define MOE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+#define MOE_OK 0
+#define MOE_ERR_ARG (-1)       /* null pointer, non-positive size, k not in [1, E], E too large */
+#define MOE_ERR_SHAPE (-2)     /* H or F not a multiple of 128, E not a multiple of 8 */
+#define MOE_ERR_ALIGN (-3)     /* a device pointer not 16-byte aligned */
+#define MOE_ERR_WORKSPACE (-4) /* workspace smaller than the size query returns */
+#define MOE_ERR_HIP (-5)       /* the HIP runtime reported an error on launch */
+
+/* limits */
+#define MOE_MAX_EXPERTS 256
+#define MOE_MAX_TOPK 32
+
+/* flags (moe_dims.flags, moe_experts_dims.flags) */
+#define MOE_F_MASK 1u    /* token_mask is given: tokens with mask 0 are not routed */
+#define MOE_F_DW_FP32 2u /* weight gradients (dW_r, dW_gate, dW_up, dW_down) are fp32, else bf16 */
+
+/* Sizes of the full block.  T tokens (T >= 1), hidden size H, E experts,
+ * expert width F, top_k experts per token. */
+typedef struct moe_dims {
+  int32_t T, H, E, F, top_k;
+  uint32_t flags;
+} moe_dims;
+
+/* Device pointers into a `saved` buffer filled by moe_fwd (see
+ * moe_saved_views).  R_cap = T * top_k rows are reserved; the routed row
+ * count R = offsets[E] <= R_cap lives on the device. */
+typedef struct moe_saved_view {
+  float* logits;      /* [T, E]      fp32 router logits (masked tokens: computed, not used) */
+  int32_t* topk_idx;  /* [T, k]      selected experts, descending logit; -1 for masked tokens */
+  float* gates;       /* [T, k]      fp32 gates, sum 1 per valid token; 0 for masked tokens */
+  int32_t* counts;    /* [E]         rows per expert */
+  int32_t* offsets;   /* [E + 1]     exclusive prefix sum of counts; offsets[E] = R */
+  int32_t* row_token; /* [R_cap]     token of row r for r < R, -1 beyond */
+  int32_t* row_of;    /* [T, k]      row of (token, slot); -1 for masked tokens */
+  void* xp;           /* [R_cap, H]  bf16 permuted tokens (rows >= R undefined) */
+  void* g;            /* [R_cap, F]  bf16 gate projection G */
+  void* u;            /* [R_cap, F]  bf16 up projection U */
+  void* a;            /* [R_cap, F]  bf16 SwiGLU activation A = silu(G) * U */
+  void* o;            /* [R_cap, H]  bf16 expert outputs O (ungated) */
+} moe_saved_view;
+
+/* Bytes of the caller-owned `saved` buffer that carries routing and
+ * activations from moe_fwd to moe_bwd.  0 if d is invalid. */
+size_t moe_saved_bytes(const moe_dims* d);
+
+/* Bytes of scratch each call needs (contents not preserved across calls).
+ * 0 if d is invalid. */
+size_t moe_fwd_workspace_bytes(const moe_dims* d);
+size_t moe_bwd_workspace_bytes(const moe_dims* d);
+
+/* Fill `view` with device pointers into `saved` (no device work).
+ * Returns MOE_OK or MOE_ERR_ARG. */
+int moe_saved_views(const moe_dims* d, void* saved, moe_saved_view* view);
+
+/* Forward of the block.
+ *   x          [T, H]  bf16 tokens
+ *   w_r        [H, E]  bf16 router weight
+ *   w_gate     [E, H, F], w_up [E, H, F], w_down [E, F, H]  bf16 expert weights
+ *   token_mask [T] uint8 (nonzero = real token) when d->flags has MOE_F_MASK,
+ *              else ignored (may be NULL)
+ *   y          [T, H]  bf16 output (masked tokens: 0)
+ *   saved      moe_saved_bytes(d) bytes, filled for moe_bwd
+ *   ws         moe_fwd_workspace_bytes(d) bytes of scratch
+ */
+int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+            const void* w_up, const void* w_down, const uint8_t* token_mask, void* y,
+            void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the block, from the `saved` buffer of the matching moe_fwd
+ * (same d, x and weights).
+ *   dy      [T, H] bf16 upstream gradient
+ *   dx      [T, H] bf16
+ *   dw_r    [H, E], dw_gate [E, H, F], dw_up [E, H, F], dw_down [E, F, H]:
+ *           bf16, or fp32 with MOE_F_DW_FP32; overwritten (not accumulated)
+ *   ws      moe_bwd_workspace_bytes(d) bytes of scratch
+ */
+int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+            const void* w_up, const void* w_down, const void* dy, const void* saved,
+            void* dx, void* dw_r, void* dw_gate, void* dw_up, void* dw_down, void* ws,
+            size_t ws_bytes, void* stream);
+
+/* One expert-parallel rank's share (§3, "Expert parallelism and topology"):
+ * the rows dispatched to this rank's E local experts, already grouped
+ * expert-major.  rows = capacity of the row buffers (rows >= 1). */
+typedef struct moe_experts_dims {
+  int32_t rows, H, E, F;
+  uint32_t flags; /* MOE_F_DW_FP32 only */
+} moe_experts_dims;
+
+/* Device pointers into an experts `saved` buffer. */
+typedef struct moe_experts_saved_view {
+  int32_t* offsets; /* [E + 1] exclusive prefix sum of counts, clamped to rows */
+  void* g;          /* [rows, F] bf16 */
+  void* u;          /* [rows, F] bf16 */
+  void* a;          /* [rows, F] bf16 */
+} moe_experts_saved_view;
+
+size_t moe_experts_saved_bytes(const moe_experts_dims* d);
+size_t moe_experts_workspace_bytes(const moe_experts_dims* d);
+int moe_experts_saved_views(const moe_experts_dims* d, void* saved, moe_experts_saved_view* view);
+
+/* Forward of the local experts.
+ *   xp      [rows, H] bf16 dispatched rows, expert-major
+ *   counts  [E] int32 on the device: rows of each local expert, in order.  Rows
+ *           past the capacity (prefix sum beyond `rows`) are dropped: not read,
+ *           not computed, not written.  Output rows past sum(counts) are not written.
+ *   o       [rows, H] bf16 expert outputs (ungated)
+ */
+int moe_experts_fwd(const moe_experts_dims* d, const void* xp, const int32_t* counts,
+                    const void* w_gate, const void* w_up, const void* w_down, void* o,
+                    void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the local experts from the matching moe_experts_fwd `saved`
+ * (which holds the row offsets; counts are not passed again).
+ *   d_o     [rows, H] bf16 gradient of o
+ *   dxp     [rows, H] bf16
+ *   dw_*    as in moe_bwd (overwritten; zero for experts with no rows)
+ */
+int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gate, const void* w_up, const void* w_down, const void* d_o,
+                    const void* saved, void* dxp, void* dw_gate, void* dw_up, void* dw_down,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* Message describing the last error on this thread ("" if none). */
+const char* moe_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int moe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_MI355X_H */

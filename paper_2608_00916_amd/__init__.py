@@ -1,0 +1,209 @@
+"""MI355X-native mixture-of-experts FFN block (forward + backward).
+
+Python binding of the C ABI in include/moe.h, with the same entry-point names.
+Torch supplies device memory and streams; the block itself runs entirely in
+the gfx950 HIP kernels of libmoe.so.  The functions here only turn tensors into
+pointers (and, in MoEBlock / MoEExperts, allocate the caller-owned buffers).
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_MAX_EXPERTS, MOE_MAX_TOPK, MoeDims,
+                   MoeError, MoeExpertsDims, MoeExpertsSavedView, MoeSavedView, check, lib)
+
+__all__ = [
+    "dims", "experts_dims", "moe_saved_bytes", "moe_fwd_workspace_bytes",
+    "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_bwd",
+    "moe_experts_saved_bytes", "moe_experts_workspace_bytes", "moe_experts_saved_views",
+    "moe_experts_fwd", "moe_experts_bwd", "moe_last_error", "moe_version",
+    "MoEBlock", "MoEExperts", "MoeError", "MOE_F_MASK", "MOE_F_DW_FP32",
+    "MOE_MAX_EXPERTS", "MOE_MAX_TOPK",
+]
+
+
+def dims(T, H, E, F, top_k, mask=False, dw_fp32=False) -> MoeDims:
+    flags = (MOE_F_MASK if mask else 0) | (MOE_F_DW_FP32 if dw_fp32 else 0)
+    return MoeDims(T, H, E, F, top_k, flags)
+
+
+def experts_dims(rows, H, E, F, dw_fp32=False) -> MoeExpertsDims:
+    return MoeExpertsDims(rows, H, E, F, MOE_F_DW_FP32 if dw_fp32 else 0)
+
+
+def _p(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _s(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def moe_last_error() -> str:
+    return lib().moe_last_error().decode()
+
+
+def moe_version() -> int:
+    return lib().moe_version()
+
+
+# ------------------------------------------------------------------ full block
+def moe_saved_bytes(d: MoeDims) -> int:
+    return lib().moe_saved_bytes(ctypes.byref(d))
+
+
+def moe_fwd_workspace_bytes(d: MoeDims) -> int:
+    return lib().moe_fwd_workspace_bytes(ctypes.byref(d))
+
+
+def moe_bwd_workspace_bytes(d: MoeDims) -> int:
+    return lib().moe_bwd_workspace_bytes(ctypes.byref(d))
+
+
+def _view(base: torch.Tensor, ptr: int, dtype, shape):
+    off = ptr - base.data_ptr()
+    n = 1
+    for s in shape:
+        n *= s
+    nbytes = n * torch.empty((), dtype=dtype).element_size()
+    return base[off:off + nbytes].view(dtype).view(shape)
+
+
+def moe_saved_views(d: MoeDims, saved: torch.Tensor) -> dict:
+    """Tensors viewing the routing and activations inside a `saved` buffer."""
+    v = MoeSavedView()
+    check(lib().moe_saved_views(ctypes.byref(d), _p(saved), ctypes.byref(v)))
+    T, H, E, F, k = d.T, d.H, d.E, d.F, d.top_k
+    R = T * k
+    i32, f32, bf = torch.int32, torch.float32, torch.bfloat16
+    return dict(
+        logits=_view(saved, v.logits, f32, (T, E)),
+        topk_idx=_view(saved, v.topk_idx, i32, (T, k)),
+        gates=_view(saved, v.gates, f32, (T, k)),
+        counts=_view(saved, v.counts, i32, (E,)),
+        offsets=_view(saved, v.offsets, i32, (E + 1,)),
+        row_token=_view(saved, v.row_token, i32, (R,)),
+        row_of=_view(saved, v.row_of, i32, (T, k)),
+        xp=_view(saved, v.xp, bf, (R, H)),
+        g=_view(saved, v.g, bf, (R, F)),
+        u=_view(saved, v.u, bf, (R, F)),
+        a=_view(saved, v.a, bf, (R, F)),
+        o=_view(saved, v.o, bf, (R, H)),
+    )
+
+
+def moe_fwd(d, x, w_r, w_gate, w_up, w_down, token_mask, y, saved, ws, stream=None):
+    check(lib().moe_fwd(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
+                        _p(token_mask), _p(y), _p(saved), _p(ws),
+                        0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
+def moe_bwd(d, x, w_r, w_gate, w_up, w_down, dy, saved, dx, dw_r, dw_gate, dw_up, dw_down, ws,
+            stream=None):
+    check(lib().moe_bwd(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down), _p(dy),
+                        _p(saved), _p(dx), _p(dw_r), _p(dw_gate), _p(dw_up), _p(dw_down), _p(ws),
+                        0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
+# ------------------------------------------------------------------ experts only
+def moe_experts_saved_bytes(d: MoeExpertsDims) -> int:
+    return lib().moe_experts_saved_bytes(ctypes.byref(d))
+
+
+def moe_experts_workspace_bytes(d: MoeExpertsDims) -> int:
+    return lib().moe_experts_workspace_bytes(ctypes.byref(d))
+
+
+def moe_experts_saved_views(d: MoeExpertsDims, saved: torch.Tensor) -> dict:
+    v = MoeExpertsSavedView()
+    check(lib().moe_experts_saved_views(ctypes.byref(d), _p(saved), ctypes.byref(v)))
+    bf = torch.bfloat16
+    return dict(offsets=_view(saved, v.offsets, torch.int32, (d.E + 1,)),
+                g=_view(saved, v.g, bf, (d.rows, d.F)), u=_view(saved, v.u, bf, (d.rows, d.F)),
+                a=_view(saved, v.a, bf, (d.rows, d.F)))
+
+
+def moe_experts_fwd(d, xp, counts, w_gate, w_up, w_down, o, saved, ws, stream=None):
+    check(lib().moe_experts_fwd(ctypes.byref(d), _p(xp), _p(counts), _p(w_gate), _p(w_up),
+                                _p(w_down), _p(o), _p(saved), _p(ws),
+                                0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
+def moe_experts_bwd(d, xp, w_gate, w_up, w_down, d_o, saved, dxp, dw_gate, dw_up, dw_down, ws,
+                    stream=None):
+    check(lib().moe_experts_bwd(ctypes.byref(d), _p(xp), _p(w_gate), _p(w_up), _p(w_down),
+                                _p(d_o), _p(saved), _p(dxp), _p(dw_gate), _p(dw_up), _p(dw_down),
+                                _p(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                _s(stream)))
+
+
+# ------------------------------------------------------------------ owners of buffers
+class MoEBlock:
+    """Caller-side buffers for one block shape: saved activations, workspaces
+    and outputs, allocated once with torch on `device`."""
+
+    def __init__(self, T, H, E, F, top_k, mask=False, dw_fp32=False, device="cuda"):
+        self.d = dims(T, H, E, F, top_k, mask, dw_fp32)
+        nb = moe_saved_bytes(self.d)
+        if nb == 0:
+            raise MoeError(_lib.MOE_ERR_ARG, moe_last_error())
+        dev = torch.device(device)
+        self.saved = torch.empty(nb, dtype=torch.uint8, device=dev)
+        ws = max(moe_fwd_workspace_bytes(self.d), moe_bwd_workspace_bytes(self.d))
+        self.ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        wdt = torch.float32 if dw_fp32 else torch.bfloat16
+        self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        self.dx = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        self.dw_r = torch.empty((H, E), dtype=wdt, device=dev)
+        self.dw_gate = torch.empty((E, H, F), dtype=wdt, device=dev)
+        self.dw_up = torch.empty((E, H, F), dtype=wdt, device=dev)
+        self.dw_down = torch.empty((E, F, H), dtype=wdt, device=dev)
+        self.views = moe_saved_views(self.d, self.saved)
+
+    def forward(self, x, w_r, w_gate, w_up, w_down, token_mask=None, stream=None):
+        moe_fwd(self.d, x, w_r, w_gate, w_up, w_down, token_mask, self.y, self.saved, self.ws, stream)
+        return self.y
+
+    def backward(self, x, w_r, w_gate, w_up, w_down, dy, stream=None):
+        moe_bwd(self.d, x, w_r, w_gate, w_up, w_down, dy, self.saved, self.dx, self.dw_r,
+                self.dw_gate, self.dw_up, self.dw_down, self.ws, stream)
+        return self.dx, self.dw_r, self.dw_gate, self.dw_up, self.dw_down
+
+
+class MoEExperts:
+    """Caller-side buffers for one expert-parallel rank's local experts."""
+
+    def __init__(self, rows, H, E, F, dw_fp32=False, device="cuda"):
+        self.d = experts_dims(rows, H, E, F, dw_fp32)
+        dev = torch.device(device)
+        self.saved = torch.empty(moe_experts_saved_bytes(self.d), dtype=torch.uint8, device=dev)
+        self.ws = torch.empty(moe_experts_workspace_bytes(self.d), dtype=torch.uint8, device=dev)
+        wdt = torch.float32 if dw_fp32 else torch.bfloat16
+        self.o = torch.empty((rows, H), dtype=torch.bfloat16, device=dev)
+        self.dxp = torch.empty((rows, H), dtype=torch.bfloat16, device=dev)
+        self.dw_gate = torch.empty((E, H, F), dtype=wdt, device=dev)
+        self.dw_up = torch.empty((E, H, F), dtype=wdt, device=dev)
+        self.dw_down = torch.empty((E, F, H), dtype=wdt, device=dev)
+        self.views = moe_experts_saved_views(self.d, self.saved)
+
+    def forward(self, xp, counts, w_gate, w_up, w_down, stream=None):
+        moe_experts_fwd(self.d, xp, counts, w_gate, w_up, w_down, self.o, self.saved, self.ws, stream)
+        return self.o
+
+    def backward(self, xp, w_gate, w_up, w_down, d_o, stream=None):
+        moe_experts_bwd(self.d, xp, w_gate, w_up, w_down, d_o, self.saved, self.dxp, self.dw_gate,
+                        self.dw_up, self.dw_down, self.ws, stream)
+        return self.dxp, self.dw_gate, self.dw_up, self.dw_down

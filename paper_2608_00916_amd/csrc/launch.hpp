@@ -1,0 +1,76 @@
+// Internal launchers of the MoE kernels (host side).  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "moe.h"
+
+namespace moe {
+
+// Operands of the grouped expert products.  Rows are grouped expert-major;
+// offsets[E+1] and tile_start[E+1] (prefix sums of rows and of 128-row tiles
+// per expert) are device arrays.
+struct ExpertArgs {
+  int rows_cap, H, E, F;
+  const bf16_t* xp;
+  const bf16_t* w_gate;
+  const bf16_t* w_up;
+  const bf16_t* w_down;
+  const int32_t* offsets;
+  const int32_t* tile_start;
+  bf16_t* g;    // forward writes, backward reads
+  bf16_t* u;
+  bf16_t* act;  // A = silu(G) * U
+};
+
+int max_row_tiles(int rows_cap, int E);
+
+// G, U, A from Xp (gate/up products + SwiGLU).
+hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s);
+// O = A W_down per expert.
+hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s);
+// dG, dU, dXp and the three weight gradients from dO.
+hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
+                              bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
+                              hipStream_t s);
+
+// ---- routing (router.hip)
+// logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
+hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
+                             int E, int k, float* logits, int32_t* topk_idx, float* gates,
+                             hipStream_t s);
+
+// ---- permutation (permute.hip)
+// Workspace ints the permutation needs for T tokens and E experts.
+int64_t permute_ws_ints(int T, int E);
+// counts, offsets, tile_start, row_token (-1 beyond R), row_of from topk_idx;
+// then xp[r] = x[row_token[r]].
+hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
+                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
+                          int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);
+// offsets (clamped to rows) and tile_start from device counts (experts path).
+hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, int32_t* offsets,
+                                      int32_t* tile_start, hipStream_t s);
+
+// ---- combine (combine.hip)
+// y[t] = sum_j gates[t,j] o[row_of[t,j]] (0 for masked tokens).
+hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
+                          int k, bf16_t* y, hipStream_t s);
+// dO[row_of[t,j]] = g dY[t]; dg = <dY[t], O[row]>; dz[t,:] (bf16, dense over E).
+hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
+                              const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
+                              int k, bf16_t* d_o, float* dg, bf16_t* dz, hipStream_t s);
+
+// ---- router backward (router_bwd.hip)
+int dwr_splits(int T);
+// dW_r = x^T dz via `dwr_splits(T)` fp32 partials in ws_f32 ([splits][H][E]).
+hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, float* ws_f32,
+                      void* dw_r, bool f32_out, hipStream_t s);
+// dX[t] = sum_j dXp[row_of[t,j]] + dz[t] W_r^T.
+hipError_t launch_router_dx(const bf16_t* dz, const bf16_t* w_r, const bf16_t* dxp,
+                            const int32_t* row_of, int T, int H, int E, int k, bf16_t* dx,
+                            hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,347 @@
+// C ABI of the MoE block (declared in include/moe.h): argument checks,
+// carving of the caller's `saved` and workspace buffers, and the launch
+// sequence of the forward and backward passes on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <initializer_list>
+#include <utility>
+
+#include "launch.hpp"
+#include "moe.h"
+
+using namespace moe;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return MOE_OK;
+}
+
+constexpr size_t kAlign = 256;
+size_t up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+// Sequential carve-up of a buffer into 256-byte aligned regions.
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* b) : base(static_cast<char*>(b)) {}
+  template <typename T>
+  T* take(size_t count) {
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += up(count * sizeof(T));
+    return p;
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_dims(const moe_dims* d) {
+  if (d == nullptr) return fail(MOE_ERR_ARG, "dims is NULL");
+  if (d->T < 1 || d->H < 1 || d->E < 1 || d->F < 1)
+    return fail(MOE_ERR_ARG, "T, H, E, F must be positive (T=%d H=%d E=%d F=%d)", d->T, d->H, d->E, d->F);
+  if (d->E > MOE_MAX_EXPERTS) return fail(MOE_ERR_ARG, "E=%d exceeds %d", d->E, MOE_MAX_EXPERTS);
+  if (d->top_k < 1 || d->top_k > d->E || d->top_k > MOE_MAX_TOPK)
+    return fail(MOE_ERR_ARG, "top_k=%d must be in [1, min(E, %d)]", d->top_k, MOE_MAX_TOPK);
+  if (d->H % 128 != 0 || d->F % 128 != 0)
+    return fail(MOE_ERR_SHAPE, "H=%d and F=%d must be multiples of 128", d->H, d->F);
+  if (d->E % 8 != 0) return fail(MOE_ERR_SHAPE, "E=%d must be a multiple of 8", d->E);
+  if (static_cast<int64_t>(d->T) * d->top_k > (1ll << 30))
+    return fail(MOE_ERR_ARG, "T*top_k=%lld too large", static_cast<long long>(d->T) * d->top_k);
+  if (d->flags & ~(MOE_F_MASK | MOE_F_DW_FP32)) return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
+  return MOE_OK;
+}
+
+int check_experts_dims(const moe_experts_dims* d) {
+  if (d == nullptr) return fail(MOE_ERR_ARG, "dims is NULL");
+  if (d->rows < 1 || d->H < 1 || d->E < 1 || d->F < 1)
+    return fail(MOE_ERR_ARG, "rows, H, E, F must be positive (rows=%d H=%d E=%d F=%d)", d->rows, d->H, d->E,
+                d->F);
+  if (d->E > MOE_MAX_EXPERTS) return fail(MOE_ERR_ARG, "E=%d exceeds %d", d->E, MOE_MAX_EXPERTS);
+  if (d->H % 128 != 0 || d->F % 128 != 0)
+    return fail(MOE_ERR_SHAPE, "H=%d and F=%d must be multiples of 128", d->H, d->F);
+  if (d->rows > (1 << 30)) return fail(MOE_ERR_ARG, "rows=%d too large", d->rows);
+  if (d->flags & ~MOE_F_DW_FP32) return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
+  return MOE_OK;
+}
+
+int check_ptrs(std::initializer_list<std::pair<const char*, const void*>> ps) {
+  for (const auto& p : ps) {
+    if (p.second == nullptr) return fail(MOE_ERR_ARG, "%s is NULL", p.first);
+    if (!aligned16(p.second)) return fail(MOE_ERR_ALIGN, "%s is not 16-byte aligned", p.first);
+  }
+  return MOE_OK;
+}
+
+// ---- layout of the block's `saved` buffer
+struct Saved {
+  float* logits;
+  int32_t *topk_idx, *counts, *offsets, *tile_start, *row_token, *row_of;
+  float* gates;
+  bf16_t *xp, *g, *u, *a, *o;
+  size_t bytes;
+};
+
+Saved saved_layout(const moe_dims* d, void* base) {
+  const size_t T = d->T, E = d->E, k = d->top_k, H = d->H, F = d->F, R = T * k;
+  Carve c(base);
+  Saved s;
+  s.logits = c.take<float>(T * E);
+  s.topk_idx = c.take<int32_t>(T * k);
+  s.gates = c.take<float>(T * k);
+  s.counts = c.take<int32_t>(E);
+  s.offsets = c.take<int32_t>(E + 1);
+  s.tile_start = c.take<int32_t>(E + 1);
+  s.row_token = c.take<int32_t>(R);
+  s.row_of = c.take<int32_t>(T * k);
+  s.xp = c.take<bf16_t>(R * H);
+  s.g = c.take<bf16_t>(R * F);
+  s.u = c.take<bf16_t>(R * F);
+  s.a = c.take<bf16_t>(R * F);
+  s.o = c.take<bf16_t>(R * H);
+  s.bytes = c.off;
+  return s;
+}
+
+size_t fwd_ws(const moe_dims* d) { return up(permute_ws_ints(d->T, d->E) * sizeof(int32_t)); }
+
+// ---- layout of the backward workspace
+struct BwdWs {
+  bf16_t* d_o;  // also dXp once dO is dead
+  bf16_t *dg, *du, *dz;
+  float *dgate, *dwr_part;
+  size_t bytes;
+};
+
+BwdWs bwd_layout(const moe_dims* d, void* base) {
+  const size_t T = d->T, E = d->E, k = d->top_k, H = d->H, F = d->F, R = T * k;
+  Carve c(base);
+  BwdWs w;
+  w.d_o = c.take<bf16_t>(R * H);
+  w.dg = c.take<bf16_t>(R * F);
+  w.du = c.take<bf16_t>(R * F);
+  w.dz = c.take<bf16_t>(T * E);
+  w.dgate = c.take<float>(T * k);
+  w.dwr_part = c.take<float>(static_cast<size_t>(dwr_splits(d->T)) * H * E);
+  w.bytes = c.off;
+  return w;
+}
+
+struct ExpSaved {
+  int32_t *offsets, *tile_start;
+  bf16_t *g, *u, *a;
+  size_t bytes;
+};
+
+ExpSaved exp_saved_layout(const moe_experts_dims* d, void* base) {
+  const size_t E = d->E, F = d->F, R = d->rows;
+  Carve c(base);
+  ExpSaved s;
+  s.offsets = c.take<int32_t>(E + 1);
+  s.tile_start = c.take<int32_t>(E + 1);
+  s.g = c.take<bf16_t>(R * F);
+  s.u = c.take<bf16_t>(R * F);
+  s.a = c.take<bf16_t>(R * F);
+  s.bytes = c.off;
+  return s;
+}
+
+struct ExpWs {
+  bf16_t *dg, *du;
+  size_t bytes;
+};
+
+ExpWs exp_ws_layout(const moe_experts_dims* d, void* base) {
+  const size_t F = d->F, R = d->rows;
+  Carve c(base);
+  ExpWs w;
+  w.dg = c.take<bf16_t>(R * F);
+  w.du = c.take<bf16_t>(R * F);
+  w.bytes = c.off;
+  return w;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t moe_saved_bytes(const moe_dims* d) {
+  if (check_dims(d) != MOE_OK) return 0;
+  return saved_layout(d, nullptr).bytes;
+}
+
+size_t moe_fwd_workspace_bytes(const moe_dims* d) {
+  if (check_dims(d) != MOE_OK) return 0;
+  return fwd_ws(d);
+}
+
+size_t moe_bwd_workspace_bytes(const moe_dims* d) {
+  if (check_dims(d) != MOE_OK) return 0;
+  return bwd_layout(d, nullptr).bytes;
+}
+
+int moe_saved_views(const moe_dims* d, void* saved, moe_saved_view* v) {
+  if (int rc = check_dims(d)) return rc;
+  if (saved == nullptr || v == nullptr) return fail(MOE_ERR_ARG, "saved or view is NULL");
+  const Saved s = saved_layout(d, saved);
+  v->logits = s.logits;
+  v->topk_idx = s.topk_idx;
+  v->gates = s.gates;
+  v->counts = s.counts;
+  v->offsets = s.offsets;
+  v->row_token = s.row_token;
+  v->row_of = s.row_of;
+  v->xp = s.xp;
+  v->g = s.g;
+  v->u = s.u;
+  v->a = s.a;
+  v->o = s.o;
+  return ok();
+}
+
+int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+            const void* w_down, const uint8_t* token_mask, void* y, void* saved, void* ws,
+            size_t ws_bytes, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"y", y}, {"saved", saved}, {"ws", ws}}))
+    return rc;
+  const bool masked = d->flags & MOE_F_MASK;
+  if (masked && token_mask == nullptr) return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
+  if (ws_bytes < fwd_ws(d))
+    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, fwd_ws(d));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Saved sv = saved_layout(d, saved);
+  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
+  const bf16_t* xb = static_cast<const bf16_t*>(x);
+  hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
+                                   E, k, sv.logits, sv.topk_idx, sv.gates, s);
+  if (e != hipSuccess) return hip_status(e, "router");
+  e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.row_token,
+                     sv.row_of, sv.xp, static_cast<int32_t*>(ws), s);
+  if (e != hipSuccess) return hip_status(e, "permute");
+  ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
+  e = launch_gateup_fwd(a, s);
+  if (e != hipSuccess) return hip_status(e, "gate/up");
+  e = launch_down_fwd(a, sv.o, s);
+  if (e != hipSuccess) return hip_status(e, "down");
+  e = launch_combine(sv.o, sv.gates, sv.row_of, T, H, k, static_cast<bf16_t*>(y), s);
+  return hip_status(e, "combine");
+}
+
+int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+            const void* w_down, const void* dy, const void* saved, void* dx, void* dw_r, void* dw_gate,
+            void* dw_up, void* dw_down, void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"dy", dy}, {"saved", saved}, {"dx", dx}, {"dw_r", dw_r}, {"dw_gate", dw_gate},
+                           {"dw_up", dw_up}, {"dw_down", dw_down}, {"ws", ws}}))
+    return rc;
+  const BwdWs w = bwd_layout(d, ws);
+  if (ws_bytes < w.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Saved sv = saved_layout(d, const_cast<void*>(saved));
+  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
+  const bool f32 = d->flags & MOE_F_DW_FP32;
+  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
+                                    T, H, E, k, w.d_o, w.dgate, w.dz, s);
+  if (e != hipSuccess) return hip_status(e, "combine bwd");
+  ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
+  // dXp reuses dO's memory: the down products that read dO are queued first.
+  e = launch_experts_bwd(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_gate, dw_up, dw_down, f32, s);
+  if (e != hipSuccess) return hip_status(e, "experts bwd");
+  e = launch_dwr(static_cast<const bf16_t*>(x), w.dz, T, H, E, w.dwr_part, dw_r, f32, s);
+  if (e != hipSuccess) return hip_status(e, "router weight grad");
+  e = launch_router_dx(w.dz, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
+                       static_cast<bf16_t*>(dx), s);
+  return hip_status(e, "dx");
+}
+
+size_t moe_experts_saved_bytes(const moe_experts_dims* d) {
+  if (check_experts_dims(d) != MOE_OK) return 0;
+  return exp_saved_layout(d, nullptr).bytes;
+}
+
+size_t moe_experts_workspace_bytes(const moe_experts_dims* d) {
+  if (check_experts_dims(d) != MOE_OK) return 0;
+  return exp_ws_layout(d, nullptr).bytes;
+}
+
+int moe_experts_saved_views(const moe_experts_dims* d, void* saved, moe_experts_saved_view* v) {
+  if (int rc = check_experts_dims(d)) return rc;
+  if (saved == nullptr || v == nullptr) return fail(MOE_ERR_ARG, "saved or view is NULL");
+  const ExpSaved s = exp_saved_layout(d, saved);
+  v->offsets = s.offsets;
+  v->g = s.g;
+  v->u = s.u;
+  v->a = s.a;
+  return ok();
+}
+
+int moe_experts_fwd(const moe_experts_dims* d, const void* xp, const int32_t* counts, const void* w_gate,
+                    const void* w_up, const void* w_down, void* o, void* saved, void* ws, size_t ws_bytes,
+                    void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (int rc = check_experts_dims(d)) return rc;
+  if (int rc = check_ptrs({{"xp", xp}, {"counts", counts}, {"w_gate", w_gate}, {"w_up", w_up},
+                           {"w_down", w_down}, {"o", o}, {"saved", saved}}))
+    return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const ExpSaved sv = exp_saved_layout(d, saved);
+  hipError_t e = launch_offsets_from_counts(counts, d->E, d->rows, sv.offsets, sv.tile_start, s);
+  if (e != hipSuccess) return hip_status(e, "offsets");
+  ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
+               static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
+               sv.g, sv.u, sv.a};
+  e = launch_gateup_fwd(a, s);
+  if (e != hipSuccess) return hip_status(e, "gate/up");
+  e = launch_down_fwd(a, static_cast<bf16_t*>(o), s);
+  return hip_status(e, "down");
+}
+
+int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gate, const void* w_up,
+                    const void* w_down, const void* d_o, const void* saved, void* dxp, void* dw_gate,
+                    void* dw_up, void* dw_down, void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_experts_dims(d)) return rc;
+  if (int rc = check_ptrs({{"xp", xp}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down}, {"d_o", d_o},
+                           {"saved", saved}, {"dxp", dxp}, {"dw_gate", dw_gate}, {"dw_up", dw_up},
+                           {"dw_down", dw_down}, {"ws", ws}}))
+    return rc;
+  const ExpWs w = exp_ws_layout(d, ws);
+  if (ws_bytes < w.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const ExpSaved sv = exp_saved_layout(d, const_cast<void*>(saved));
+  ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
+               static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
+               sv.g, sv.u, sv.a};
+  hipError_t e = launch_experts_bwd(a, static_cast<const bf16_t*>(d_o), w.dg, w.du, static_cast<bf16_t*>(dxp),
+                                    dw_gate, dw_up, dw_down, (d->flags & MOE_F_DW_FP32) != 0, s);
+  return hip_status(e, "experts bwd");
+}
+
+const char* moe_last_error(void) { return g_err; }
+
+int moe_version(void) { return 100; }
+
+}  // extern "C"

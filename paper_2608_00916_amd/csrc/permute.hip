@@ -1,0 +1,194 @@
+// Token permutation of the MoE block: a stable counting sort of the routed
+// (token, slot) pairs into expert-major, token-ascending rows, then a
+// coalesced gather of the token rows.  All integer work is exact and
+// deterministic: per-chunk expert membership is a bitmask built with LDS
+// atomic ORs (order-independent), and a pair's rank inside its chunk is a
+// popcount of the bits of lower tokens.
+#include <algorithm>
+
+#include "launch.hpp"
+
+namespace moe {
+
+namespace {
+
+constexpr int kChunk = 256;  // tokens per workgroup (4 waves x 64 lanes)
+constexpr int kWords = kChunk / 64;
+
+// bits[e][w] bit l  <=>  token chunk*256 + 64 w + l selected expert e.
+__device__ __forceinline__ void build_bits(unsigned long long (*bits)[kWords], const int32_t* topk_idx,
+                                           int T, int E, int k, int chunk) {
+  for (int i = threadIdx.x; i < E * kWords; i += kChunk) bits[i / kWords][i % kWords] = 0ull;
+  __syncthreads();
+  const int t = chunk * kChunk + threadIdx.x;
+  if (t < T) {
+    const unsigned long long bit = 1ull << (threadIdx.x & 63);
+    for (int j = 0; j < k; ++j) {
+      const int e = topk_idx[static_cast<int64_t>(t) * k + j];
+      if (e >= 0) atomicOr(&bits[e][threadIdx.x >> 6], bit);
+    }
+  }
+  __syncthreads();
+}
+
+// Per chunk: rows of each expert; also marks every row_token slot unused (-1).
+__global__ __launch_bounds__(kChunk) void k_perm_hist(const int32_t* __restrict__ topk_idx, int T, int E,
+                                                      int k, int32_t* __restrict__ chunk_counts,
+                                                      int32_t* __restrict__ row_token) {
+  __shared__ unsigned long long bits[MOE_MAX_EXPERTS][kWords];
+  const int chunk = blockIdx.x;
+  const int t = chunk * kChunk + threadIdx.x;
+  if (t < T)
+    for (int j = 0; j < k; ++j) row_token[static_cast<int64_t>(t) * k + j] = -1;
+  build_bits(bits, topk_idx, T, E, k, chunk);
+  for (int e = threadIdx.x; e < E; e += kChunk) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kWords; ++w) c += __popcll(bits[e][w]);
+    chunk_counts[static_cast<int64_t>(chunk) * E + e] = c;
+  }
+}
+
+// Exclusive scan of n values held one per thread (n <= blockDim = 256).
+__device__ __forceinline__ int block_exclusive_scan(int v, int* tmp) {
+  const int tid = threadIdx.x;
+  tmp[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int add = tid >= off ? tmp[tid - off] : 0;
+    __syncthreads();
+    tmp[tid] += add;
+    __syncthreads();
+  }
+  const int incl = tmp[tid];
+  __syncthreads();
+  return incl - v;
+}
+
+// One workgroup: counts[e], offsets = exclusive scan (E+1), tile_start of
+// 128-row tiles (E+1), and chunk_base[c][e] = offsets[e] + rows of expert e
+// in chunks before c.
+__global__ __launch_bounds__(256) void k_perm_scan(const int32_t* __restrict__ chunk_counts, int nchunks,
+                                                   int E, int32_t* __restrict__ chunk_base,
+                                                   int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                                                   int32_t* __restrict__ tile_start) {
+  __shared__ int tmp[256];
+  const int e = threadIdx.x;
+  int running = 0;
+  if (e < E)
+    for (int c = 0; c < nchunks; ++c) {
+      const int64_t i = static_cast<int64_t>(c) * E + e;
+      const int v = chunk_counts[i];
+      chunk_base[i] = running;
+      running += v;
+    }
+  const int n = e < E ? running : 0;
+  const int off = block_exclusive_scan(n, tmp);
+  const int tiles = cdiv(n, 128);
+  const int toff = block_exclusive_scan(tiles, tmp);
+  if (e < E) {
+    counts[e] = n;
+    offsets[e] = off;
+    tile_start[e] = toff;
+    for (int c = 0; c < nchunks; ++c) chunk_base[static_cast<int64_t>(c) * E + e] += off;
+  }
+  if (e == E - 1) {
+    offsets[E] = off + n;
+    tile_start[E] = toff + tiles;
+  }
+}
+
+__global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restrict__ topk_idx, int T, int E,
+                                                         int k, const int32_t* __restrict__ chunk_base,
+                                                         int32_t* __restrict__ row_token,
+                                                         int32_t* __restrict__ row_of) {
+  __shared__ unsigned long long bits[MOE_MAX_EXPERTS][kWords];
+  const int chunk = blockIdx.x;
+  build_bits(bits, topk_idx, T, E, k, chunk);
+  const int t = chunk * kChunk + threadIdx.x;
+  if (t >= T) return;
+  const int w = threadIdx.x >> 6;
+  const unsigned long long below = (1ull << (threadIdx.x & 63)) - 1ull;
+  for (int j = 0; j < k; ++j) {
+    const int64_t p = static_cast<int64_t>(t) * k + j;
+    const int e = topk_idx[p];
+    if (e < 0) {
+      row_of[p] = -1;
+      continue;
+    }
+    int rank = __popcll(bits[e][w] & below);
+    for (int ww = 0; ww < w; ++ww) rank += __popcll(bits[e][ww]);
+    const int r = chunk_base[static_cast<int64_t>(chunk) * E + e] + rank;
+    row_token[r] = t;
+    row_of[p] = r;
+  }
+}
+
+// xp[r] = x[row_token[r]] for r < offsets[E]; 16 bytes per thread.
+__global__ __launch_bounds__(256) void k_gather(const bf16_t* __restrict__ x,
+                                                const int32_t* __restrict__ row_token,
+                                                const int32_t* __restrict__ offsets, int E, int H,
+                                                bf16_t* __restrict__ xp) {
+  const int64_t R = offsets[E];
+  const int cpr = H / 8;  // 16-byte chunks per row
+  const int64_t n = R * cpr;
+  for (int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; q < n;
+       q += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t r = q / cpr;
+    const int c = static_cast<int>(q - r * cpr);
+    const int64_t t = row_token[r];
+    *reinterpret_cast<uint4*>(xp + r * H + c * 8) = *reinterpret_cast<const uint4*>(x + t * H + c * 8);
+  }
+}
+
+// Experts path: offsets from device counts, clamped to the row capacity.
+__global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __restrict__ counts, int E,
+                                                             int rows, int32_t* __restrict__ offsets,
+                                                             int32_t* __restrict__ tile_start) {
+  __shared__ int tmp[256];
+  const int e = threadIdx.x;
+  const int c = e < E ? max(0, counts[e]) : 0;
+  const int off = block_exclusive_scan(c, tmp);
+  const int lo = min(off, rows), hi = min(off + c, rows);
+  const int n = hi - lo;
+  const int tiles = cdiv(n, 128);
+  const int toff = block_exclusive_scan(tiles, tmp);
+  if (e < E) {
+    offsets[e] = lo;
+    tile_start[e] = toff;
+  }
+  if (e == E - 1) {
+    offsets[E] = hi;
+    tile_start[E] = toff + tiles;
+  }
+}
+
+}  // namespace
+
+int64_t permute_ws_ints(int T, int E) { return 2 * static_cast<int64_t>(cdiv(T, kChunk)) * E; }
+
+hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
+                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
+                          int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
+  const int nchunks = cdiv(T, kChunk);
+  int32_t* chunk_counts = ws;
+  int32_t* chunk_base = ws + static_cast<int64_t>(nchunks) * E;
+  hipLaunchKernelGGL(k_perm_hist, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts,
+                     row_token);
+  hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(256), 0, s, chunk_counts, nchunks, E, chunk_base, counts,
+                     offsets, tile_start);
+  hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
+                     row_token, row_of);
+  const int64_t work = static_cast<int64_t>(T) * k * (H / 8);
+  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(work, 256), 4096));
+  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, x, row_token, offsets, E, H, xp);
+  return hipGetLastError();
+}
+
+hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, int32_t* offsets,
+                                      int32_t* tile_start, hipStream_t s) {
+  hipLaunchKernelGGL(k_offsets_from_counts, dim3(1), dim3(256), 0, s, counts, E, rows, offsets, tile_start);
+  return hipGetLastError();
+}
+
+}  // namespace moe
