@@ -1,0 +1,193 @@
+#!/usr/bin/env python3
+"""Throughput of the MoE block, forward + backward, on one MI355X.
+
+One step = moe_fwd + moe_bwd over one batch of the workload (router, top-k,
+permutation, SwiGLU expert products, combine, and the whole backward), inputs
+resident in HBM before the timed region.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload qwen3_30b_a3b]
+
+The workload defaults to the Qwen3-30B-A3B-shaped layer on one GPU (T=8192
+tokens, H=2048, E=128 experts, top-8, F=768, bf16).  The dominant kernel's
+roofline comes from HIP events recorded around every library kernel launch
+over the timed region; the CPU baseline is the fp64 oracle on a bounded
+sample of the same workload, timed on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+import workloads
+
+METRIC = "MoE block fwd+bwd tokens/sec and TFLOP/s (% bf16 MFMA peak), 1 MI355X"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def kernel_work(name, T, Tv, H, E, F, k, R):
+    """Algorithmic work of one launch of each kernel: (kind, amount).
+    FLOP for matrix products, bytes for data-movement kernels."""
+    b = 2  # bf16
+    return {
+        "router_logits": ("flop", 2.0 * T * H * E),
+        "gateup_fwd": ("flop", 4.0 * H * F * R),
+        "down_fwd": ("flop", 2.0 * H * F * R),
+        "down_dgrad_swiglu": ("flop", 2.0 * H * F * R),
+        "down_wgrad": ("flop", 2.0 * H * F * R),
+        "gateup_dgrad": ("flop", 4.0 * H * F * R),
+        "gateup_wgrad": ("flop", 4.0 * H * F * R),
+        "dwr_partial": ("flop", 2.0 * Tv * H * E),
+        "router_dx": ("flop", 2.0 * Tv * H * E),
+        "gather": ("byte", float(Tv * H * b + R * H * b)),
+        "combine": ("byte", float(R * H * b + Tv * H * b)),
+        "combine_bwd": ("byte", float(Tv * H * b + 2 * R * H * b)),
+    }.get(name, ("none", 0.0))
+
+
+def cpu_baseline(inp, k, tokens):
+    """The fp64 oracle, as it stands, on the first `tokens` tokens."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import moe_oracle as O
+    w = {n: O.widen_bf16(inp[n]) for n in ("w_r", "w_gate", "w_up", "w_down")}
+    x = O.widen_bf16(inp["x"][:tokens])
+    dy = O.widen_bf16(inp["dy"][:tokens])
+    mask = None if inp["mask"] is None else inp["mask"][:tokens].astype(bool)
+    t0 = time.perf_counter()
+    f = O.moe_forward(x, w["w_r"], w["w_gate"], w["w_up"], w["w_down"], k, mask)
+    O.moe_backward(x, w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, dy)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {tokens} of {inp['dims']['T']} tokens of the same workload "
+                      f"(all {inp['dims']['E']} experts' weights), one fwd+bwd, fp64, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3_30b_a3b",
+                    choices=[n for n, c in workloads.CONFIGS.items() if c["kind"] == "block"])
+    ap.add_argument("--cpu-tokens", type=int, default=2048,
+                    help="tokens of the oracle's CPU-baseline sample (0 = skip)")
+    ap.add_argument("--no-trace", action="store_true",
+                    help="do not record per-kernel events in the timed region")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the block runs on a single MI355X and this build has "
+              f"no multi-GPU path (--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_00916_amd as moe
+
+    cfg = workloads.CONFIGS[args.workload]
+    inp = workloads.make(args.workload)
+    d = inp["dims"]
+    T, H, E, F, k = d["T"], d["H"], d["E"], d["F"], d["k"]
+    mask_np = inp["mask"]
+    Tv = T if mask_np is None else int(mask_np.sum())
+    R = Tv * k
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    t = {n: dev(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    tm = None if mask_np is None else torch.from_numpy(mask_np.astype(np.uint8)).cuda()
+    blk = moe.MoEBlock(T, H, E, F, k, mask=tm is not None)
+
+    def step():
+        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {args.workload}: warmup {args.warmup} done", file=sys.stderr, flush=True)
+
+    moe.moe_trace_read()  # drop anything recorded before
+    if not args.no_trace:
+        moe.moe_trace_enable(True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    moe.moe_trace_enable(False)
+    ms = ev0.elapsed_time(ev1) / args.steps
+    kern = moe.moe_trace_read()
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})",
+          file=sys.stderr, flush=True)
+
+    gemm_flop = 18.0 * H * F * R
+    router_flop = 6.0 * H * E * Tv
+    tflops = (gemm_flop + router_flop) / (ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": Tv / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload} MoE block fwd+bwd", "T": T, "T_valid": Tv, "H": H,
+                   "E": E, "top_k": k, "F": F, "routed_rows": R, "seed": cfg["seed"]},
+        "block_tflops": tflops,
+        "block_frac_bf16_peak": tflops / PEAK_BF16_TFLOPS,
+    }
+    if kern:
+        per = {}
+        for name, (tot, n) in kern.items():
+            avg_ms = tot / n
+            kind, amt = kernel_work(name, T, Tv, H, E, F, k, R)
+            row = {"avg_us": round(avg_ms * 1e3, 2), "launches": n}
+            if kind == "flop":
+                row["tflops"] = round(amt / (avg_ms * 1e-3) / 1e12, 1)
+            elif kind == "byte":
+                row["gbs"] = round(amt / (avg_ms * 1e-3) / 1e9, 1)
+            per[name] = row
+        out["kernels"] = per
+        gemm_names = ("gateup_fwd", "down_fwd", "down_dgrad_swiglu", "down_wgrad", "gateup_dgrad",
+                      "gateup_wgrad")
+        gemm_ms = sum(kern[n][0] / kern[n][1] for n in gemm_names if n in kern)
+        out["grouped_gemm_frac_bf16_peak"] = gemm_flop / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+        dom = max(kern, key=lambda n: kern[n][0])
+        tot, n = kern[dom]
+        avg_s = tot / n * 1e-3
+        kind, amt = kernel_work(dom, T, Tv, H, E, F, k, R)
+        if kind == "flop":
+            ach = amt / avg_s / 1e12
+            out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                               "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None}
+        else:
+            ach = amt / avg_s / 1e9
+            out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                               "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None}
+    if args.cpu_tokens > 0:
+        print(f"[bench] CPU baseline: oracle on {args.cpu_tokens} tokens", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(inp, k, min(args.cpu_tokens, T))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -172,6 +172,17 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
                     const void* saved, void* dxp, void* dw_gate, void* dw_up, void* dw_down,
                     void* ws, size_t ws_bytes, void* stream);
 
+/* Per-kernel timing.  With tracing on, every kernel the library launches is
+ * bracketed by two HIP events recorded on its launch stream (no host
+ * synchronisation at launch time).  moe_trace_read waits for the recorded
+ * events, writes per kernel id the summed milliseconds and the number of
+ * launches since the last read (arrays of n entries; either may be NULL), and
+ * returns the number of kernel ids (or MOE_ERR_HIP).  moe_trace_name(id) is a
+ * kernel's name ("" for an unknown id).  Not thread-safe; off by default. */
+int moe_trace_enable(int on);
+int moe_trace_read(double* total_ms, int32_t* launches, int n);
+const char* moe_trace_name(int id);
+
 /* Message describing the last error on this thread ("" if none). */
 const char* moe_last_error(void);
 

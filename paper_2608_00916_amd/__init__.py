@@ -20,7 +20,7 @@ __all__ = [
     "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_bwd",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes", "moe_experts_saved_views",
     "moe_experts_fwd", "moe_experts_bwd", "moe_last_error", "moe_version",
-    "MoEBlock", "MoEExperts", "MoeError", "MOE_F_MASK", "MOE_F_DW_FP32",
+    "moe_trace_enable", "moe_trace_read", "MoEBlock", "MoEExperts", "MoeError", "MOE_F_MASK", "MOE_F_DW_FP32",
     "MOE_MAX_EXPERTS", "MOE_MAX_TOPK",
 ]
 
@@ -58,6 +58,22 @@ def moe_last_error() -> str:
 
 def moe_version() -> int:
     return lib().moe_version()
+
+
+def moe_trace_enable(on: bool) -> None:
+    check(lib().moe_trace_enable(1 if on else 0))
+
+
+def moe_trace_read() -> dict:
+    """{kernel name: (total ms, launches)} since the last read (waits for the
+    recorded events)."""
+    n = 64
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int32 * n)()
+    m = lib().moe_trace_read(ms, cnt, n)
+    if m < 0:
+        check(m)
+    return {lib().moe_trace_name(i).decode(): (ms[i], cnt[i]) for i in range(m) if cnt[i]}
 
 
 # ------------------------------------------------------------------ full block

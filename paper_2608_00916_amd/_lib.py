@@ -27,6 +27,7 @@ EXPORTS = (
     "moe_saved_views", "moe_fwd", "moe_bwd",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes",
     "moe_experts_saved_views", "moe_experts_fwd", "moe_experts_bwd",
+    "moe_trace_enable", "moe_trace_read", "moe_trace_name",
     "moe_last_error", "moe_version",
 )
 
@@ -86,6 +87,10 @@ def lib() -> ctypes.CDLL:
         "moe_experts_saved_views": (ctypes.c_int, [ED, P, ctypes.POINTER(MoeExpertsSavedView)]),
         "moe_experts_fwd": (ctypes.c_int, [ED, P, P, P, P, P, P, P, P, S, P]),
         "moe_experts_bwd": (ctypes.c_int, [ED, P, P, P, P, P, P, P, P, P, P, P, S, P]),
+        "moe_trace_enable": (ctypes.c_int, [ctypes.c_int]),
+        "moe_trace_read": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_int32), ctypes.c_int]),
+        "moe_trace_name": (ctypes.c_char_p, [ctypes.c_int]),
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_version": (ctypes.c_int, []),
     }

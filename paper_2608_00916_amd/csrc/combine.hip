@@ -2,6 +2,7 @@
 // the router-logit gradient dz).  One wave per token; rows move as 16-byte
 // vectors (8 bf16 per lane), sums are fp32 in slot order.
 #include "launch.hpp"
+#include "trace.hpp"
 
 namespace moe {
 
@@ -106,15 +107,21 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ 
 
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s) {
-  hipLaunchKernelGGL(k_combine, dim3(cdiv(T, 4)), dim3(256), 0, s, o, gates, row_of, T, H, k, y);
+  {
+    TraceScope trace_scope(K_COMBINE, s);
+    hipLaunchKernelGGL(k_combine, dim3(cdiv(T, 4)), dim3(256), 0, s, o, gates, row_of, T, H, k, y);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
                               const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
                               int k, bf16_t* d_o, float* dg, bf16_t* dz, hipStream_t s) {
-  hipLaunchKernelGGL(k_combine_bwd, dim3(cdiv(T, 4)), dim3(256), 0, s, dy, o, gates, topk_idx, row_of, T,
-                     H, E, k, d_o, dg, dz);
+  {
+    TraceScope trace_scope(K_COMBINE_BWD, s);
+    hipLaunchKernelGGL(k_combine_bwd, dim3(cdiv(T, 4)), dim3(256), 0, s, dy, o, gates, topk_idx, row_of, T,
+                       H, E, k, d_o, dg, dz);
+  }
   return hipGetLastError();
 }
 

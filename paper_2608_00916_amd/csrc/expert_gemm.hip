@@ -8,6 +8,7 @@
 // (K = rows of one expert) have a fixed grid of E x (M/128) x (N/128) tiles;
 // experts without rows write zeros.
 #include "launch.hpp"
+#include "trace.hpp"
 #include "gemm_core.hpp"
 
 #include <algorithm>
@@ -284,16 +285,22 @@ int max_row_tiles(int rows_cap, int E) { return cdiv(rows_cap, BM) + E; }
 hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s) {
   const int grid =
       persistent_grid(k_gateup_fwd, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / BN));
-  hipLaunchKernelGGL(k_gateup_fwd, dim3(grid), dim3(kThreads), 0, s, a.xp, a.w_gate, a.w_up, a.offsets,
-                     a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
+  {
+    TraceScope trace_scope(K_GATEUP_FWD, s);
+    hipLaunchKernelGGL(k_gateup_fwd, dim3(grid), dim3(kThreads), 0, s, a.xp, a.w_gate, a.w_up, a.offsets,
+                       a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   const int grid =
       persistent_grid(k_down_fwd, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / BN));
-  hipLaunchKernelGGL(k_down_fwd, dim3(grid), dim3(kThreads), 0, s, a.act, a.w_down, a.offsets,
-                     a.tile_start, a.E, a.H, a.F, o);
+  {
+    TraceScope trace_scope(K_DOWN_FWD, s);
+    hipLaunchKernelGGL(k_down_fwd, dim3(grid), dim3(kThreads), 0, s, a.act, a.w_down, a.offsets,
+                       a.tile_start, a.E, a.H, a.F, o);
+  }
   return hipGetLastError();
 }
 
@@ -301,26 +308,38 @@ hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg
                               bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
                               hipStream_t s) {
   const int64_t tiles = max_row_tiles(a.rows_cap, a.E);
-  hipLaunchKernelGGL(k_down_dgrad_swiglu, dim3(persistent_grid(k_down_dgrad_swiglu, tiles * (a.F / BN))),
-                     dim3(kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start, a.E, a.H,
-                     a.F, dg, du);
+  {
+    TraceScope trace_scope(K_DOWN_DGRAD, s);
+    hipLaunchKernelGGL(k_down_dgrad_swiglu, dim3(persistent_grid(k_down_dgrad_swiglu, tiles * (a.F / BN))),
+                       dim3(kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start, a.E, a.H,
+                       a.F, dg, du);
+  }
   const int gw_down = grid8(static_cast<int64_t>(a.E) * (a.F / BM) * (a.H / BN));
-  if (dw_f32)
+  if (dw_f32) {
+    TraceScope trace_scope(K_DOWN_WGRAD, s);
     hipLaunchKernelGGL(k_down_wgrad<true>, dim3(gw_down), dim3(kThreads), 0, s, a.act, d_o, a.offsets,
                        a.E, a.H, a.F, dw_down);
-  else
+  } else {
+    TraceScope trace_scope(K_DOWN_WGRAD, s);
     hipLaunchKernelGGL(k_down_wgrad<false>, dim3(gw_down), dim3(kThreads), 0, s, a.act, d_o, a.offsets,
                        a.E, a.H, a.F, dw_down);
-  hipLaunchKernelGGL(k_gateup_dgrad, dim3(persistent_grid(k_gateup_dgrad, tiles * (a.H / BN))),
-                     dim3(kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start, a.E, a.H,
-                     a.F, dxp);
+  }
+  {
+    TraceScope trace_scope(K_GATEUP_DGRAD, s);
+    hipLaunchKernelGGL(k_gateup_dgrad, dim3(persistent_grid(k_gateup_dgrad, tiles * (a.H / BN))),
+                       dim3(kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start, a.E, a.H,
+                       a.F, dxp);
+  }
   const int gw_gu = grid8(static_cast<int64_t>(a.E) * (a.H / BM) * (a.F / BN));
-  if (dw_f32)
+  if (dw_f32) {
+    TraceScope trace_scope(K_GATEUP_WGRAD, s);
     hipLaunchKernelGGL(k_gateup_wgrad<true>, dim3(gw_gu), dim3(kThreads), 0, s, a.xp, dg, du, a.offsets,
                        a.E, a.H, a.F, dw_gate, dw_up);
-  else
+  } else {
+    TraceScope trace_scope(K_GATEUP_WGRAD, s);
     hipLaunchKernelGGL(k_gateup_wgrad<false>, dim3(gw_gu), dim3(kThreads), 0, s, a.xp, dg, du,
                        a.offsets, a.E, a.H, a.F, dw_gate, dw_up);
+  }
   return hipGetLastError();
 }
 

@@ -7,6 +7,7 @@
 #include <algorithm>
 
 #include "launch.hpp"
+#include "trace.hpp"
 
 namespace moe {
 
@@ -173,21 +174,36 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
   const int nchunks = cdiv(T, kChunk);
   int32_t* chunk_counts = ws;
   int32_t* chunk_base = ws + static_cast<int64_t>(nchunks) * E;
-  hipLaunchKernelGGL(k_perm_hist, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts,
-                     row_token);
-  hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(256), 0, s, chunk_counts, nchunks, E, chunk_base, counts,
-                     offsets, tile_start);
-  hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
-                     row_token, row_of);
+  {
+    TraceScope trace_scope(K_PERM_HIST, s);
+    hipLaunchKernelGGL(k_perm_hist, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts,
+                       row_token);
+  }
+  {
+    TraceScope trace_scope(K_PERM_SCAN, s);
+    hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(256), 0, s, chunk_counts, nchunks, E, chunk_base, counts,
+                       offsets, tile_start);
+  }
+  {
+    TraceScope trace_scope(K_PERM_SCATTER, s);
+    hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
+                       row_token, row_of);
+  }
   const int64_t work = static_cast<int64_t>(T) * k * (H / 8);
   const int grid = static_cast<int>(std::min<int64_t>(cdiv64(work, 256), 4096));
-  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, x, row_token, offsets, E, H, xp);
+  {
+    TraceScope trace_scope(K_GATHER, s);
+    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, x, row_token, offsets, E, H, xp);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, int32_t* offsets,
                                       int32_t* tile_start, hipStream_t s) {
-  hipLaunchKernelGGL(k_offsets_from_counts, dim3(1), dim3(256), 0, s, counts, E, rows, offsets, tile_start);
+  {
+    TraceScope trace_scope(K_OFFSETS, s);
+    hipLaunchKernelGGL(k_offsets_from_counts, dim3(1), dim3(256), 0, s, counts, E, rows, offsets, tile_start);
+  }
   return hipGetLastError();
 }
 

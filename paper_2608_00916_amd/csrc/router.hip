@@ -5,6 +5,7 @@
 
 #include "gemm_core.hpp"
 #include "launch.hpp"
+#include "trace.hpp"
 
 namespace moe {
 
@@ -112,9 +113,15 @@ __global__ __launch_bounds__(256) void k_topk(const float* __restrict__ logits,
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
                              int E, int k, float* logits, int32_t* topk_idx, float* gates,
                              hipStream_t s) {
-  hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, BM), cdiv(E, BN)), dim3(kThreads), 0, s, x, w_r, T, H,
-                     E, logits);
-  hipLaunchKernelGGL(k_topk, dim3(cdiv(T, 4)), dim3(256), 0, s, logits, mask, T, E, k, topk_idx, gates);
+  {
+    TraceScope trace_scope(K_ROUTER_LOGITS, s);
+    hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, BM), cdiv(E, BN)), dim3(kThreads), 0, s, x, w_r, T, H,
+                       E, logits);
+  }
+  {
+    TraceScope trace_scope(K_TOPK, s);
+    hipLaunchKernelGGL(k_topk, dim3(cdiv(T, 4)), dim3(256), 0, s, logits, mask, T, E, k, topk_idx, gates);
+  }
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 
 #include "gemm_core.hpp"
 #include "launch.hpp"
+#include "trace.hpp"
 
 namespace moe {
 
@@ -105,22 +106,31 @@ int dwr_splits(int T) { return cdiv(T, kDwrChunk); }
 hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, float* ws_f32,
                       void* dw_r, bool f32_out, hipStream_t s) {
   const int splits = dwr_splits(T);
-  hipLaunchKernelGGL(k_dwr_partial, dim3(splits, H / BM, cdiv(E, BN)), dim3(kThreads), 0, s, x, dz, T, H,
-                     E, ws_f32);
+  {
+    TraceScope trace_scope(K_DWR_PARTIAL, s);
+    hipLaunchKernelGGL(k_dwr_partial, dim3(splits, H / BM, cdiv(E, BN)), dim3(kThreads), 0, s, x, dz, T, H,
+                       E, ws_f32);
+  }
   const int64_t n = static_cast<int64_t>(H) * E;
   const int grid = static_cast<int>(std::min<int64_t>(cdiv64(n, 256), 2048));
-  if (f32_out)
+  if (f32_out) {
+    TraceScope trace_scope(K_DWR_REDUCE, s);
     hipLaunchKernelGGL(k_dwr_reduce<true>, dim3(grid), dim3(256), 0, s, ws_f32, splits, n, dw_r);
-  else
+  } else {
+    TraceScope trace_scope(K_DWR_REDUCE, s);
     hipLaunchKernelGGL(k_dwr_reduce<false>, dim3(grid), dim3(256), 0, s, ws_f32, splits, n, dw_r);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_router_dx(const bf16_t* dz, const bf16_t* w_r, const bf16_t* dxp,
                             const int32_t* row_of, int T, int H, int E, int k, bf16_t* dx,
                             hipStream_t s) {
-  hipLaunchKernelGGL(k_router_dx, dim3(cdiv(T, BM), H / BN), dim3(kThreads), 0, s, dz, w_r, dxp, row_of, T,
-                     H, E, k, dx);
+  {
+    TraceScope trace_scope(K_ROUTER_DX, s);
+    hipLaunchKernelGGL(k_router_dx, dim3(cdiv(T, BM), H / BN), dim3(kThreads), 0, s, dz, w_r, dxp, row_of, T,
+                       H, E, k, dx);
+  }
   return hipGetLastError();
 }
 

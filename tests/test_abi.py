@@ -1,0 +1,139 @@
+"""The C ABI without a GPU: the header compiles as C, the library loads and
+exports every function the header declares, size queries are consistent, and
+every argument error is reported before any device work is launched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_00916_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_\w+)\s*\(", text)))
+
+
+def test_header_compiles_as_c():
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def test_library_exports_every_declared_function():
+    L = _lib.lib()
+    names = declared_functions()
+    assert len(names) >= 16
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(_lib.EXPORTS)
+
+
+def D(T=256, H=128, E=8, F=256, k=2, flags=0):
+    return _lib.MoeDims(T, H, E, F, k, flags)
+
+
+def test_size_queries():
+    L = _lib.lib()
+    d = D()
+    saved = L.moe_saved_bytes(ctypes.byref(d))
+    R = 256 * 2
+    # at least Xp, G, U, A, O and the routing tables
+    assert saved >= R * (128 * 2 * 2 + 256 * 2 * 3) + 256 * 8 * 4
+    assert L.moe_fwd_workspace_bytes(ctypes.byref(d)) > 0
+    assert L.moe_bwd_workspace_bytes(ctypes.byref(d)) >= R * 128 * 2 + 2 * R * 256 * 2
+    # sizes grow with T and are 0 for invalid dims
+    assert L.moe_saved_bytes(ctypes.byref(D(T=512))) > saved
+    assert L.moe_saved_bytes(ctypes.byref(D(H=100))) == 0
+    ed = _lib.MoeExpertsDims(1000, 256, 4, 128, 0)
+    assert L.moe_experts_saved_bytes(ctypes.byref(ed)) >= 3 * 1000 * 128 * 2
+    assert L.moe_experts_workspace_bytes(ctypes.byref(ed)) >= 2 * 1000 * 128 * 2
+    assert L.moe_version() >= 100
+
+
+def test_saved_views_are_disjoint_and_aligned():
+    L = _lib.lib()
+    d = D()
+    base = 1 << 20
+    v = _lib.MoeSavedView()
+    assert L.moe_saved_views(ctypes.byref(d), base, ctypes.byref(v)) == 0
+    ptrs = [getattr(v, n) for n, _ in _lib.MoeSavedView._fields_]
+    assert all(p % 256 == 0 for p in ptrs)
+    assert len(set(ptrs)) == len(ptrs) and sorted(ptrs) == ptrs
+    assert ptrs[-1] < base + L.moe_saved_bytes(ctypes.byref(d))
+
+
+FAKE = 1 << 24  # aligned, never dereferenced: every call below fails its checks first
+
+
+def fwd(d, **over):
+    a = dict(x=FAKE, w_r=FAKE, w_gate=FAKE, w_up=FAKE, w_down=FAKE, mask=None, y=FAKE, saved=FAKE,
+             ws=FAKE, ws_bytes=1 << 40)
+    a.update(over)
+    L = _lib.lib()
+    return L.moe_fwd(ctypes.byref(d), a["x"], a["w_r"], a["w_gate"], a["w_up"], a["w_down"], a["mask"],
+                     a["y"], a["saved"], a["ws"], a["ws_bytes"], None)
+
+
+def bwd(d, **over):
+    a = dict(x=FAKE, w_r=FAKE, w_gate=FAKE, w_up=FAKE, w_down=FAKE, dy=FAKE, saved=FAKE, dx=FAKE,
+             dw_r=FAKE, dw_gate=FAKE, dw_up=FAKE, dw_down=FAKE, ws=FAKE, ws_bytes=1 << 40)
+    a.update(over)
+    L = _lib.lib()
+    return L.moe_bwd(ctypes.byref(d), a["x"], a["w_r"], a["w_gate"], a["w_up"], a["w_down"], a["dy"],
+                     a["saved"], a["dx"], a["dw_r"], a["dw_gate"], a["dw_up"], a["dw_down"], a["ws"],
+                     a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("dims,code", [
+    (D(T=0), _lib.MOE_ERR_ARG),
+    (D(k=0), _lib.MOE_ERR_ARG),
+    (D(k=9), _lib.MOE_ERR_ARG),                 # k > E
+    (D(E=264, k=2), _lib.MOE_ERR_ARG),          # E above the limit
+    (D(E=64, k=33), _lib.MOE_ERR_ARG),          # k above the limit
+    (D(H=100), _lib.MOE_ERR_SHAPE),
+    (D(F=200), _lib.MOE_ERR_SHAPE),
+    (D(E=12), _lib.MOE_ERR_SHAPE),
+    (D(flags=8), _lib.MOE_ERR_ARG),
+])
+def test_bad_dims(dims, code):
+    assert fwd(dims) == code
+    assert bwd(dims) == code
+    assert _lib.lib().moe_last_error().decode() != ""
+
+
+def test_bad_pointers_and_workspace():
+    d = D()
+    assert fwd(d, x=None) == _lib.MOE_ERR_ARG
+    assert "x is NULL" in _lib.lib().moe_last_error().decode()
+    assert fwd(d, w_down=FAKE + 8) == _lib.MOE_ERR_ALIGN
+    assert fwd(D(flags=_lib.MOE_F_MASK)) == _lib.MOE_ERR_ARG  # mask flag without mask
+    assert fwd(d, ws_bytes=0) == _lib.MOE_ERR_WORKSPACE
+    assert bwd(d, dy=None) == _lib.MOE_ERR_ARG
+    assert bwd(d, dw_r=FAKE + 4) == _lib.MOE_ERR_ALIGN
+    assert bwd(d, ws_bytes=1024) == _lib.MOE_ERR_WORKSPACE
+    L = _lib.lib()
+    ed = _lib.MoeExpertsDims(100, 128, 4, 128, 0)
+    assert L.moe_experts_fwd(ctypes.byref(ed), FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0,
+                             None) == _lib.MOE_ERR_ARG
+    bad = _lib.MoeExpertsDims(100, 128, 4, 100, 0)
+    assert L.moe_experts_fwd(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0,
+                             None) == _lib.MOE_ERR_SHAPE
+    assert L.moe_experts_bwd(ctypes.byref(ed), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                             FAKE, FAKE, 16, None) == _lib.MOE_ERR_WORKSPACE
+
+
+def test_trace_api_without_launches():
+    L = _lib.lib()
+    assert L.moe_trace_enable(0) == 0
+    n = L.moe_trace_read(None, None, 0)
+    assert n >= 17
+    names = {L.moe_trace_name(i).decode() for i in range(n)}
+    assert {"gateup_fwd", "gateup_wgrad", "combine", "topk"} <= names
+    assert L.moe_trace_name(-1).decode() == ""
