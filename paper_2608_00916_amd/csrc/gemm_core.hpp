@@ -1,209 +1,353 @@
 // bf16 MFMA GEMM core shared by every matrix product of the MoE block.
 //
-// One workgroup (256 threads = 4 waves of 64, arranged 2 x 2) computes a
-// BM x BN fp32 tile C = A_tile * B_tile over a K loop in steps of BK:
+// One workgroup (WM x WN waves of 64 lanes) computes a BM x BN fp32 tile C = A_tile * B_tile over a K loop in steps of BK = 64:
 //   C[m][n] = sum_k A(m, k) B(k, n)
 // Operands come from global memory in one of two layouts:
 //   K-contiguous   element (r, k) at src[r * ld + k]   (a row-major A, or B^T)
 //   MN-contiguous  element (r, k) at src[k * ld + r]   (a row-major B, or A^T)
-// Both are staged in LDS as [rows][BK] bf16 with K contiguous (128-byte rows,
-// 16-byte chunks XOR-swizzled by row so that the MFMA operand reads and the
-// tile writes are free of bank conflicts).  MN-contiguous tiles are read as
-// 8 x 8 blocks of 16-byte rows and transposed in registers on the way in.
+// Both are copied to LDS untouched (16-byte buffer loads staged through
+// registers): a K-contiguous tile as [rows][64] (128-byte rows), an
+// MN-contiguous tile as [64][rows].  16-byte units are XOR-swizzled by row so
+// that both the tile writes and the MFMA operand reads are free of bank
+// conflicts.  The MFMA wants 8 consecutive k per lane: K-contiguous tiles give
+// them with one ds_read_b128; MN-contiguous tiles with two
+// ds_read_b64_tr_b16, the gfx950 LDS read that transposes 4 x 4 blocks of
+// 16-bit elements across groups of four lanes.
 //
-// LDS holds two stages: the global loads of step k+1 are in flight while the
-// MFMAs of step k run, with one barrier per step.
+// Two LDS stages and two register sets: the global loads of step k+2 are in
+// flight while the MFMAs of step k run, with one LDS-only barrier per step.
 //
-// MFMA v_mfma_f32_16x16x32_bf16 is fed with the B tile as its first operand
-// and the A tile as its second, so that each lane ends up holding four
+// v_mfma_f32_16x16x32_bf16 is fed with the B tile as its first operand and
+// the A tile as its second, so that each lane ends up holding four
 // consecutive columns of one output row:
-//   lane l, fragment (mi, ni), register i  ->  C[mb + mi*16 + l%16][nb + ni*16 + 4*(l/16) + i]
+//   lane l, fragment (mi, ni), register i -> C[row(mi) + l%16][col(ni) + 4 (l/16) + i]
+//
+// With NB = 2 the B tile holds two operands side by side (columns [0, BN/2)
+// from the first, [BN/2, BN) from the second) and each wave takes matching
+// columns of both, so an epilogue can combine them element by element.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 
 namespace moe {
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kThreads = 256;
-constexpr int WTM = BM / 2, WTN = BN / 2;  // wave tile 64 x 64
-constexpr int FM = WTM / 16, FN = WTN / 16;
-constexpr int kTileBytes = 128 * BK * 2;   // one 128-row LDS operand tile (16 KiB)
+constexpr int BK = 64;
 
-// Byte offset of 16-byte chunk `chunk` (0..7) of LDS row `row`.
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * (BK * 2) + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 4);
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define MOE_LDS __attribute__((address_space(3)))
+
+// BM x BN tile computed by WM x WN waves (each (BM/WM) x (BN/WN)).
+template <int BM_, int BN_, int NB_, int WM_ = 2, int WN_ = 2>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, NB = NB_, WM = WM_, WN = WN_;
+  static constexpr int kThreads = 64 * WM * WN;
+  static constexpr int FM = BM / WM / 16;  // 16-row A fragments per wave
+  static constexpr int FN = BN / WN / 16;  // 16-row B fragments per wave
+  static constexpr int BNS = BN / NB;      // rows of one B operand in the tile
+  static constexpr int kABytes = BM * BK * 2;
+  static constexpr int kBBytes = BN * BK * 2;
+  static constexpr int kStage = kABytes + kBBytes;
+  static constexpr int kLds = 2 * kStage;
+};
+
+// ---------------------------------------------------------------- LDS layouts
+// K-contiguous tile [rows][64]: byte offset of 16-byte chunk c (0..7) of row r.
+__device__ __forceinline__ int kc_off(int r, int c) { return r * 128 + ((c ^ ((r ^ (r >> 3)) & 7)) << 4); }
+
+// MN-contiguous tile [64][ROWS]: byte offset of 16-byte unit u of k-row k.
+// The XOR moves 32-byte blocks so that the 16 rows one transposing read
+// touches (k = 8 g + j, g, j < 4) land in distinct banks.
+template <int ROWS>
+__device__ __forceinline__ int mn_off(int k, int u) {
+  const int h = (k & 3) | (((k >> 3) & 1) << 2);
+  return k * (ROWS * 2) + ((u ^ (h << 1)) << 4);
 }
 
-// K-contiguous 128 x BK tile.  Rows >= r_lim and k >= k_lim read as zero
-// (k_lim is a multiple of 8).
+// ---------------------------------------------------------------- global -> registers -> LDS
+// Global loads go through buffer resources: a lane whose byte offset is at or
+// beyond the resource's size reads zeros, so ragged rows and K tails need no
+// branches.  Each K step moves the resource base by one step; offsets are
+// fixed per lane.
+constexpr uint32_t kOob = 0x80000000u;  // an offset beyond every resource size
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int n = static_cast<int>(bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes));
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, n, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
+}
+
+// K-contiguous operand: ROWS tile rows starting at LDS row `row0`.  Rows
+// >= r_lim and k >= K read as zero (K a multiple of 8).
+template <int ROWS, int kThreads>
 struct LoadKc {
-  static constexpr int kPer = 128 * (BK / 8) / kThreads;  // 4 chunks per thread
-  uint4 v[kPer];
-  __device__ __forceinline__ void load(const bf16_t* src, int64_t ld, int r_lim, int k0, int k_lim,
-                                       int tid) {
+  static constexpr int kPer = ROWS * (BK / 8) / kThreads;
+  static_assert(kPer * kThreads == ROWS * (BK / 8), "tile rows must split evenly over the threads");
+  const char* base;
+  int64_t valid;  // bytes of the r_lim valid rows
+  int64_t ld2;    // row pitch in bytes
+  uint32_t off[kPer];
+  __device__ __forceinline__ void init(const bf16_t* src, int64_t ld, int r_lim, int tid) {
+    base = reinterpret_cast<const char*>(src);
+    ld2 = ld * 2;
+    valid = r_lim > 0 ? static_cast<int64_t>(r_lim) * ld2 : 0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int q = i * kThreads + tid;
-      const int row = q >> 3, k = k0 + ((q & 7) << 3);
-      if (row < r_lim && k < k_lim)
-        v[i] = *reinterpret_cast<const uint4*>(src + row * ld + k);
-      else
-        v[i] = make_uint4(0, 0, 0, 0);
+      off[i] = static_cast<uint32_t>((q >> 3) * ld2 + ((q & 7) << 4));
     }
   }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
+  __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int K, int tid) const {
+    const int64_t step = static_cast<int64_t>(kt) * (BK * 2);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base + step, valid - step);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int q = i * kThreads + tid;
-      *reinterpret_cast<uint4*>(lds + lds_off(q >> 3, q & 7)) = v[i];
+      const bool kin = kt * BK + ((q & 7) << 3) < K;
+      v[i] = buf_load16(r, kin ? off[i] : kOob);
+    }
+  }
+  __device__ __forceinline__ void store(const uint4 (&v)[kPer], char* lds, int row0, int tid) const {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int q = i * kThreads + tid;
+      *reinterpret_cast<uint4*>(lds + kc_off(row0 + (q >> 3), q & 7)) = v[i];
     }
   }
 };
 
-// MN-contiguous 128 x BK tile, transposed into the K-contiguous LDS layout.
-// Thread tid < 128 owns the 8 x 8 block (rows rb*8.., k kb*8..) with
-// rb = tid % 16 and kb = tid / 16, so that 16 neighbouring lanes read 256
-// contiguous bytes of one k row.  Rows >= r_lim (a multiple of 8) and
-// k >= k_lim read as zero.
-struct LoadMNc {
-  uint4 v[8];
-  __device__ __forceinline__ void load(const bf16_t* src, int64_t ld, int r_lim, int k0, int k_lim,
-                                       int tid) {
-    if (tid >= 128) return;
-    const int rb = tid & 15, kb = tid >> 4;
-    const bool rok = rb * 8 < r_lim;
+// MN-contiguous operand: ROWS columns of the tile's [64][TROWS] LDS layout
+// starting at column `col0`.  Columns >= r_lim (a multiple of 8) and k >= K
+// read as zero.
+template <int ROWS, int TROWS, int kThreads>
+struct LoadMn {
+  static constexpr int kUnits = ROWS / 8;  // 16-byte units per k-row
+  static constexpr int kPer = BK * kUnits / kThreads;
+  static_assert(kPer * kThreads == BK * kUnits, "tile columns must split evenly over the threads");
+  const char* base;
+  int64_t valid;  // bytes of the K valid k-rows
+  int64_t ld2;
+  uint32_t off[kPer];
+  __device__ __forceinline__ void init(const bf16_t* src, int64_t ld, int r_lim, int K, int tid) {
+    base = reinterpret_cast<const char*>(src);
+    ld2 = ld * 2;
+    valid = K > 0 ? static_cast<int64_t>(K) * ld2 : 0;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const int k = k0 + kb * 8 + s;
-      if (rok && k < k_lim)
-        v[s] = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(k) * ld + rb * 8);
-      else
-        v[s] = make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < kPer; ++i) {
+      const int q = i * kThreads + tid;
+      const int k = q / kUnits, u = q % kUnits;
+      off[i] = u * 8 < r_lim ? static_cast<uint32_t>(k * ld2 + u * 16) : kOob;
     }
   }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
-    if (tid >= 128) return;
-    const int rb = tid & 15, kb = tid >> 4;
-    const uint32_t* in = reinterpret_cast<const uint32_t*>(v);  // in[s*4 + w]: k = s, rows 2w, 2w+1
+  __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int, int) const {
+    const int64_t step = static_cast<int64_t>(kt) * BK * ld2;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(base + step, valid - step);
 #pragma unroll
-    for (int m = 0; m < 8; ++m) {
-      uint32_t o[4];
+    for (int i = 0; i < kPer; ++i) v[i] = buf_load16(r, off[i]);
+  }
+  __device__ __forceinline__ void store(const uint4 (&v)[kPer], char* lds, int col0, int tid) const {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const uint32_t a = in[(2 * p) * 4 + (m >> 1)];      // k = 2p
-        const uint32_t b = in[(2 * p + 1) * 4 + (m >> 1)];  // k = 2p + 1
-        o[p] = (m & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
-      }
-      *reinterpret_cast<uint4*>(lds + lds_off(rb * 8 + m, kb)) = make_uint4(o[0], o[1], o[2], o[3]);
+    for (int i = 0; i < kPer; ++i) {
+      const int q = i * kThreads + tid;
+      const int k = q / kUnits, u = q % kUnits;
+      *reinterpret_cast<uint4*>(lds + mn_off<TROWS>(k, (col0 >> 3) + u)) = v[i];
     }
   }
 };
 
-template <bool KC>
-struct Loader;
-template <>
-struct Loader<true> : LoadKc {};
-template <>
-struct Loader<false> : LoadMNc {};
+template <bool KC, int ROWS, int TROWS, int NT>
+struct Loader : LoadKc<ROWS, NT> {
+  __device__ __forceinline__ void setup(const bf16_t* src, int64_t ld, int r_lim, int, int tid) {
+    this->init(src, ld, r_lim, tid);
+  }
+};
+template <int ROWS, int TROWS, int NT>
+struct Loader<false, ROWS, TROWS, NT> : LoadMn<ROWS, TROWS, NT> {
+  __device__ __forceinline__ void setup(const bf16_t* src, int64_t ld, int r_lim, int K, int tid) {
+    this->init(src, ld, r_lim, K, tid);
+  }
+};
 
-// Accumulate one BK step of the wave's 64 x 64 sub-tile(s) from LDS.
-template <int NB>
-__device__ __forceinline__ void mma_step(const char* a_lds, const char* const* b_lds, int wm, int wn,
-                                         int lane, f32x4 (&acc)[NB][FM][FN]) {
-#pragma unroll
-  for (int ks = 0; ks < BK / 32; ++ks) {
-    const int chunk = ks * 4 + (lane >> 4);
-    uint4 af[FM];
-#pragma unroll
-    for (int mi = 0; mi < FM; ++mi)
-      af[mi] = *reinterpret_cast<const uint4*>(a_lds + lds_off(wm * WTM + mi * 16 + (lane & 15), chunk));
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      uint4 bfr[FN];
-#pragma unroll
-      for (int ni = 0; ni < FN; ++ni)
-        bfr[ni] = *reinterpret_cast<const uint4*>(b_lds[b] + lds_off(wn * WTN + ni * 16 + (lane & 15), chunk));
-#pragma unroll
-      for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < FN; ++ni) acc[b][mi][ni] = mfma16x16x32(bfr[ni], af[mi], acc[b][mi][ni]);
-    }
+// Barrier for LDS traffic only: waits for this wave's LDS operations, then
+// for every wave, without draining global loads still in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// ---------------------------------------------------------------- LDS -> MFMA operands
+// 16 x 32 operand fragment (rows rbase..rbase+15, k = ks*32 .. ks*32+31):
+// lane l gets row rbase + l%16, k = ks*32 + 8 (l/16) + 0..7.
+template <bool KC, int TROWS>
+__device__ __forceinline__ uint4 frag(const char* lds, int rbase, int ks, int lane) {
+  if constexpr (KC) {
+    return *reinterpret_cast<const uint4*>(lds + kc_off(rbase + (lane & 15), ks * 4 + (lane >> 4)));
+  } else {
+    const int s = lane & 15, g = lane >> 4;
+    const int k = ks * 32 + 8 * g + (s >> 2);
+    const int n = rbase + 4 * (s & 3);
+    const int o = (n & 7) * 2;
+    const MOE_LDS char* base = (const MOE_LDS char*)(lds);
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (MOE_LDS v4i16*)(base + mn_off<TROWS>(k, n >> 3) + o));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (MOE_LDS v4i16*)(base + mn_off<TROWS>(k + 4, n >> 3) + o));
+    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    return make_uint4(a.x, a.y, b.x, b.y);
   }
 }
 
-template <int NB>
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[NB][FM][FN]) {
-#pragma unroll
-  for (int b = 0; b < NB; ++b)
-#pragma unroll
-    for (int mi = 0; mi < FM; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < FN; ++ni) acc[b][mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+// First B-tile row of wave column wn's fragment ni.  With NB = 2 the first
+// FN/2 fragments come from the first operand's columns, the rest from the
+// matching columns of the second.
+template <class C>
+__device__ __forceinline__ int brow(int wn, int ni) {
+  if constexpr (C::NB == 1) {
+    return wn * (C::BN / C::WN) + ni * 16;
+  } else {
+    constexpr int half = C::FN / 2;
+    constexpr int span = C::BN / 2 / C::WN;
+    return (ni < half) ? wn * span + ni * 16 : C::BN / 2 + wn * span + (ni - half) * 16;
+  }
 }
 
-// LDS bytes the main loop needs for NB B operands.
-template <int NB>
-constexpr int mainloop_lds_bytes() {
-  return 2 * (1 + NB) * kTileBytes;
+// Operand fragments of one 32-deep slice ks of the LDS stage.
+template <class C, bool A_KC, bool B_KC>
+__device__ __forceinline__ void read_frags(const char* a_lds, const char* b_lds, int wm, int wn, int ks,
+                                           int lane, uint4 (&af)[C::FM], uint4 (&bf)[C::FN]) {
+#pragma unroll
+  for (int mi = 0; mi < C::FM; ++mi) af[mi] = frag<A_KC, C::BM>(a_lds, wm * (C::BM / C::WM) + mi * 16, ks, lane);
+#pragma unroll
+  for (int ni = 0; ni < C::FN; ++ni) bf[ni] = frag<B_KC, C::BN>(b_lds, brow<C>(wn, ni), ks, lane);
 }
 
-// acc[b] += A(0:BM, 0:K) * B_b(0:K, 0:BN).
-//   a      tile origin: (m0, k = 0) of A, layout per A_KC, leading dim lda
-//   m_lim  valid rows of the tile (<= BM); k_lim = K (number of valid k)
-//   b[i]   tile origins of the NB B operands, layout per B_KC, leading dim ldb
-//   n_lim  valid columns (multiple of 8)
-template <bool A_KC, bool B_KC, int NB>
+template <class C>
+__device__ __forceinline__ void mfmas(const uint4 (&af)[C::FM], const uint4 (&bf)[C::FN],
+                                      f32x4 (&acc)[C::FM][C::FN]) {
+#pragma unroll
+  for (int mi = 0; mi < C::FM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < C::FN; ++ni) acc[mi][ni] = mfma16x16x32(bf[ni], af[mi], acc[mi][ni]);
+}
+
+template <class C>
+__device__ __forceinline__ void zero_acc(f32x4 (&acc)[C::FM][C::FN]) {
+#pragma unroll
+  for (int mi = 0; mi < C::FM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < C::FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// acc += A(0:BM, 0:K) * [B_0 | B_1](0:K, 0:BN).
+//   a      tile origin (m0, k = 0) of A in layout A_KC, leading dimension lda
+//   m_lim  valid rows of the tile (<= BM); K = number of valid k
+//   b[i]   tile origins of the NB B operands in layout B_KC, leading dim ldb
+//   n_lim  valid columns of each B operand (multiple of 8)
+// Software pipeline: global loads run two K steps ahead of the MFMAs in two
+// register sets; LDS holds two stages; one LDS barrier per step.
+template <class C, bool A_KC, bool B_KC>
 __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int m_lim,
                                               const bf16_t* const* b, int64_t ldb, int n_lim, int K,
-                                              char* smem, f32x4 (&acc)[NB][FM][FN]) {
+                                              char* smem, f32x4 (&acc)[C::FM][C::FN]) {
+  using LA = Loader<A_KC, C::BM, C::BM, C::kThreads>;
+  using LB = Loader<B_KC, C::BNS, C::BN, C::kThreads>;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  constexpr int kStage = (1 + NB) * kTileBytes;
-  Loader<A_KC> la;
-  Loader<B_KC> lb[NB];
+  const int wm = wave / C::WN, wn = wave % C::WN;
   const int nk = cdiv(K, BK);
   if (nk <= 0) return;
+  LA la;
+  LB lb[C::NB];
+  la.setup(a, lda, m_lim, K, tid);
+#pragma unroll
+  for (int i = 0; i < C::NB; ++i) lb[i].setup(b[i], ldb, n_lim, K, tid);
+  uint4 ra[2][LA::kPer];
+  uint4 rb[2][C::NB][LB::kPer];
 
-  la.load(a, lda, m_lim, 0, K, tid);
+  auto load = [&](auto set, int kt) {
+    constexpr int S = decltype(set)::value;
+    la.load(ra[S], kt, K, tid);
 #pragma unroll
-  for (int i = 0; i < NB; ++i) lb[i].load(b[i], ldb, n_lim, 0, K, tid);
-  la.store(smem, tid);
+    for (int i = 0; i < C::NB; ++i) lb[i].load(rb[S][i], kt, K, tid);
+  };
+  auto store = [&](auto set, char* stage) {
+    constexpr int S = decltype(set)::value;
+    la.store(ra[S], stage, 0, tid);
 #pragma unroll
-  for (int i = 0; i < NB; ++i) lb[i].store(smem + (1 + i) * kTileBytes, tid);
-  __syncthreads();
+    for (int i = 0; i < C::NB; ++i) lb[i].store(rb[S][i], stage + C::kABytes, i * C::BNS, tid);
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  // Instruction counts of one K step, for the interleaving below.
+  constexpr int kReads = C::FM * (A_KC ? 1 : 2) + C::FN * (B_KC ? 1 : 2);  // per 32-deep slice
+  constexpr int kMfma = C::FM * C::FN;                                      // per slice
+  constexpr int kWrites = LA::kPer + C::NB * LB::kPer;
+  constexpr int kLoads = kWrites;
+  static_assert(kReads <= kMfma, "slice reads must fit between the MFMAs of a slice");
+  // One K step on LDS stage `set`: MFMAs of both 32-deep slices, the refill of
+  // the other stage from the other register set (step kt + 1, loaded two steps
+  // ago) and the global loads of step kt + 3 into that register set.  Loads
+  // past K read zeros without touching memory, so the body has no branches
+  // and the scheduler can interleave: slice-0 fragment reads, then slice-0
+  // MFMAs alternating with slice-1 fragment reads, then slice-1 MFMAs
+  // alternating with the LDS writes and global loads.
+  auto step = [&](auto set, int kt) {
+    constexpr int S = decltype(set)::value;
+    using Other = std::integral_constant<int, 1 - S>;
+    const char* cur = smem + S * C::kStage;
+    char* nxt = smem + (1 - S) * C::kStage;
+    uint4 af0[C::FM], bf0[C::FN], af1[C::FM], bf1[C::FN];
+    read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 0, lane, af0, bf0);
+    read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 1, lane, af1, bf1);
+    mfmas<C>(af0, bf0, acc);
+    mfmas<C>(af1, bf1, acc);
+    store(Other{}, nxt);
+    load(Other{}, kt + 3);
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);  // slice-0 reads
+#pragma unroll
+    for (int i = 0; i < kReads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // slice-1 read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+#pragma unroll
+    for (int i = 0; i < kWrites; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+    }
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kWrites - kLoads, 0);
+    lds_barrier();
+  };
+  static_assert(kWrites + kLoads <= kMfma, "refill must fit between the MFMAs of a slice");
 
-  for (int kt = 0; kt < nk; ++kt) {
-    char* cur = smem + (kt & 1) * kStage;
-    char* nxt = smem + ((kt + 1) & 1) * kStage;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(a, lda, m_lim, (kt + 1) * BK, K, tid);
-#pragma unroll
-      for (int i = 0; i < NB; ++i) lb[i].load(b[i], ldb, n_lim, (kt + 1) * BK, K, tid);
-    }
-    const char* bl[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) bl[i] = cur + (1 + i) * kTileBytes;
-    mma_step<NB>(cur, bl, wm, wn, lane, acc);
-    if (more) {
-      la.store(nxt, tid);
-#pragma unroll
-      for (int i = 0; i < NB; ++i) lb[i].store(nxt + (1 + i) * kTileBytes, tid);
-    }
-    __syncthreads();
+  load(S0{}, 0);
+  load(S1{}, 1);
+  store(S0{}, smem);
+  lds_barrier();
+  load(S0{}, 2);
+  for (int kt = 0; kt < nk; kt += 2) {
+    step(S0{}, kt);
+    if (kt + 1 < nk) step(S1{}, kt + 1);
   }
 }
 
-// Output coordinates of fragment (mi, ni) for this lane: row, first of 4 columns.
+// Output coordinates of fragment (mi, ni) for this lane: row, first of 4 columns
+// (columns index the B tile: [0, BN/2) first operand, [BN/2, BN) second when NB = 2).
+template <class C>
 __device__ __forceinline__ int frag_row(int mi, int lane) {
-  const int wm = (threadIdx.x >> 6) >> 1;
-  return wm * WTM + mi * 16 + (lane & 15);
+  const int wm = (threadIdx.x >> 6) / C::WN;
+  return wm * (C::BM / C::WM) + mi * 16 + (lane & 15);
 }
+template <class C>
 __device__ __forceinline__ int frag_col(int ni, int lane) {
-  const int wn = (threadIdx.x >> 6) & 1;
-  return wn * WTN + ni * 16 + 4 * (lane >> 4);
+  const int wn = (threadIdx.x >> 6) % C::WN;
+  return brow<C>(wn, ni) + 4 * (lane >> 4);
 }
 
 __device__ __forceinline__ uint2 pack4_bf16(const f32x4& v) {

@@ -12,26 +12,28 @@ namespace moe {
 namespace {
 
 // z[T,E] = x[T,H] W_r[H,E]; tile 128 tokens x 128 experts, K = H.
-__global__ __launch_bounds__(kThreads) void k_router_logits(const bf16_t* __restrict__ x,
+using RouterTile = Tile<128, 128, 1>;
+__global__ __launch_bounds__(RouterTile::kThreads) void k_router_logits(const bf16_t* __restrict__ x,
                                                             const bf16_t* __restrict__ w_r, int T, int H,
                                                             int E, float* __restrict__ logits) {
-  __shared__ __attribute__((aligned(16))) char smem[mainloop_lds_bytes<1>()];
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  f32x4 acc[1][FM][FN];
-  zero_acc<1>(acc);
+  using C = RouterTile;
+  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
+  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
+  f32x4 acc[C::FM][C::FN];
+  zero_acc<C>(acc);
   const bf16_t* bs[1] = {w_r + n0};  // B(k = h, n = e) = W_r[h][e]: E-contiguous
-  gemm_mainloop<true, false, 1>(x + static_cast<int64_t>(m0) * H, H, min(BM, T - m0), bs, E, E - n0, H,
+  gemm_mainloop<C, true, false>(x + static_cast<int64_t>(m0) * H, H, min(C::BM, T - m0), bs, E, E - n0, H,
                                 smem, acc);
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int mi = 0; mi < FM; ++mi) {
-    const int t = m0 + frag_row(mi, lane);
+  for (int mi = 0; mi < C::FM; ++mi) {
+    const int t = m0 + frag_row<C>(mi, lane);
     if (t >= T) continue;
 #pragma unroll
-    for (int ni = 0; ni < FN; ++ni) {
-      const int e = n0 + frag_col(ni, lane);
+    for (int ni = 0; ni < C::FN; ++ni) {
+      const int e = n0 + frag_col<C>(ni, lane);
       if (e >= E) continue;  // E % 8 == 0, so e < E covers e..e+3
-      const f32x4 v = acc[0][mi][ni];
+      const f32x4 v = acc[mi][ni];
       *reinterpret_cast<float4*>(logits + static_cast<int64_t>(t) * E + e) = make_float4(v[0], v[1], v[2], v[3]);
     }
   }
@@ -115,7 +117,7 @@ hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* 
                              hipStream_t s) {
   {
     TraceScope trace_scope(K_ROUTER_LOGITS, s);
-    hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, BM), cdiv(E, BN)), dim3(kThreads), 0, s, x, w_r, T, H,
+    hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, RouterTile::BM), cdiv(E, RouterTile::BN)), dim3(RouterTile::kThreads), 0, s, x, w_r, T, H,
                        E, logits);
   }
   {
