@@ -24,77 +24,113 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
                     pack_bf16x2(f[6], f[7]));
 }
 
+// Slot counts are a compile-time bound KT >= k (a power of two), so every
+// lane issues the loads of all of its token's rows before it needs them.
+
 // y[t] = sum_j g[t,j] o[row_of[t,j]]  (0 when the token has no rows).
+template <int KT>
 __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, const float* __restrict__ gates,
                                                  const int32_t* __restrict__ row_of, int T, int H, int k,
                                                  bf16_t* __restrict__ y) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const int32_t* rows = row_of + static_cast<int64_t>(t) * k;
-  const float* g = gates + static_cast<int64_t>(t) * k;
-  for (int c = lane * 8; c < H; c += kWave * 8) {
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < k; ++j) {
-      const int r = rows[j];
-      if (r < 0) continue;
-      float f[8];
-      unpack8(*reinterpret_cast<const uint4*>(o + static_cast<int64_t>(r) * H + c), f);
-      const float gj = g[j];
+  int rows[KT];
+  float g[KT];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] += gj * f[i];
+  for (int j = 0; j < KT; ++j) {
+    rows[j] = j < k ? row_of[static_cast<int64_t>(t) * k + j] : -1;
+    g[j] = j < k ? gates[static_cast<int64_t>(t) * k + j] : 0.0f;
+  }
+  for (int c = lane * 8; c < H; c += kWave * 8) {
+    uint4 v[KT];
+#pragma unroll
+    for (int j = 0; j < KT; ++j)
+      v[j] = rows[j] >= 0 ? *reinterpret_cast<const uint4*>(o + static_cast<int64_t>(rows[j]) * H + c)
+                          : make_uint4(0, 0, 0, 0);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      float f[8];
+      unpack8(v[j], f);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] += g[j] * f[i];
     }
     *reinterpret_cast<uint4*>(y + static_cast<int64_t>(t) * H + c) = pack8(acc);
   }
 }
 
 // Per token t with rows r_j:
-//   dO[r_j] = g_j dY[t]               (bf16)
-//   dg_j    = <dY[t], O[r_j]>         (fp32)
-//   dz[t,e] = g_j (dg_j - sum_j' g_j' dg_j') for e = idx_j, else 0  (bf16, all E)
+//   dO[r_j]   = g_j dY[t]                                   (bf16)
+//   dg_j      = <dY[t], O[r_j]>                              (fp32)
+//   dz_j      = g_j (dg_j - sum_j' g_j' dg_j')               (fp32, per slot)
+//   dz[t, :]  = dz_j at e = idx_j, else 0                    (bf16, all E)
+template <int KT>
 __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ dy,
                                                      const bf16_t* __restrict__ o,
                                                      const float* __restrict__ gates,
                                                      const int32_t* __restrict__ topk_idx,
                                                      const int32_t* __restrict__ row_of, int T, int H,
                                                      int E, int k, bf16_t* __restrict__ d_o,
-                                                     float* __restrict__ dg_out, bf16_t* __restrict__ dz) {
+                                                     float* __restrict__ dg_out, float* __restrict__ dz_slot,
+                                                     bf16_t* __restrict__ dz) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const int32_t* rows = row_of + static_cast<int64_t>(t) * k;
-  const float* g = gates + static_cast<int64_t>(t) * k;
+  int rows[KT];
+  float g[KT], part[KT];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    rows[j] = j < k ? row_of[static_cast<int64_t>(t) * k + j] : -1;
+    g[j] = j < k ? gates[static_cast<int64_t>(t) * k + j] : 0.0f;
+    part[j] = 0.0f;
+  }
   const bf16_t* dyr = dy + static_cast<int64_t>(t) * H;
-  float my_dg = 0.0f;  // lane j keeps dg_j
-  for (int j = 0; j < k; ++j) {
-    const int r = rows[j];
-    if (r < 0) continue;
-    const float gj = g[j];
-    float part = 0.0f;
-    for (int c = lane * 8; c < H; c += kWave * 8) {
-      float fy[8], fo[8], out[8];
-      unpack8(*reinterpret_cast<const uint4*>(dyr + c), fy);
-      unpack8(*reinterpret_cast<const uint4*>(o + static_cast<int64_t>(r) * H + c), fo);
+  for (int c = lane * 8; c < H; c += kWave * 8) {
+    const uint4 wy = *reinterpret_cast<const uint4*>(dyr + c);
+    uint4 v[KT];
+#pragma unroll
+    for (int j = 0; j < KT; ++j)
+      v[j] = rows[j] >= 0 ? *reinterpret_cast<const uint4*>(o + static_cast<int64_t>(rows[j]) * H + c)
+                          : make_uint4(0, 0, 0, 0);
+    float fy[8];
+    unpack8(wy, fy);
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      if (rows[j] < 0) continue;
+      float fo[8], out[8];
+      unpack8(v[j], fo);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        part += fy[i] * fo[i];
-        out[i] = gj * fy[i];
+        part[j] += fy[i] * fo[i];
+        out[i] = g[j] * fy[i];
       }
-      *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(r) * H + c) = pack8(out);
+      *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(rows[j]) * H + c) = pack8(out);
     }
-    const float dgj = wave_sum(part);
-    if (lane == j) my_dg = dgj;
   }
-  const float my_g = lane < k ? g[lane] : 0.0f;
+  float my_dg = 0.0f;  // lane j keeps dg_j
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    const float d = wave_sum(part[j]);
+    if (lane == j) my_dg = d;
+  }
+  float my_g = 0.0f;
+#pragma unroll
+  for (int j = 0; j < KT; ++j)
+    if (lane == j) my_g = g[j];
   const int my_e = lane < k ? topk_idx[static_cast<int64_t>(t) * k + lane] : -1;
   const float inner = wave_sum(my_g * my_dg);
   const float my_dz = my_g * (my_dg - inner);
-  if (lane < k) dg_out[static_cast<int64_t>(t) * k + lane] = my_dg;
+  if (lane < k) {
+    dg_out[static_cast<int64_t>(t) * k + lane] = my_dg;
+    dz_slot[static_cast<int64_t>(t) * k + lane] = my_dz;
+  }
   bf16_t* dzr = dz + static_cast<int64_t>(t) * E;
   for (int e0 = 0; e0 < E; e0 += kWave) {
     const int e = e0 + lane;
     float v = 0.0f;
-    for (int j = 0; j < k; ++j) {
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
       const int ej = __shfl(my_e, j, kWave);
       const float dzj = __shfl(my_dz, j, kWave);
       if (ej == e) v = dzj;
@@ -105,22 +141,32 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ 
 
 }  // namespace
 
+#define MOE_SLOT_DISPATCH(KERNEL, k, grid, s, ...)                                        \
+  do {                                                                                     \
+    if ((k) <= 1) hipLaunchKernelGGL(KERNEL<1>, grid, dim3(256), 0, s, __VA_ARGS__);       \
+    else if ((k) <= 2) hipLaunchKernelGGL(KERNEL<2>, grid, dim3(256), 0, s, __VA_ARGS__);  \
+    else if ((k) <= 4) hipLaunchKernelGGL(KERNEL<4>, grid, dim3(256), 0, s, __VA_ARGS__);  \
+    else if ((k) <= 8) hipLaunchKernelGGL(KERNEL<8>, grid, dim3(256), 0, s, __VA_ARGS__);  \
+    else if ((k) <= 16) hipLaunchKernelGGL(KERNEL<16>, grid, dim3(256), 0, s, __VA_ARGS__); \
+    else hipLaunchKernelGGL(KERNEL<32>, grid, dim3(256), 0, s, __VA_ARGS__);               \
+  } while (0)
+
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s) {
   {
     TraceScope trace_scope(K_COMBINE, s);
-    hipLaunchKernelGGL(k_combine, dim3(cdiv(T, 4)), dim3(256), 0, s, o, gates, row_of, T, H, k, y);
+    MOE_SLOT_DISPATCH(k_combine, k, dim3(cdiv(T, 4)), s, o, gates, row_of, T, H, k, y);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
                               const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, bf16_t* dz, hipStream_t s) {
+                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz, hipStream_t s) {
   {
     TraceScope trace_scope(K_COMBINE_BWD, s);
-    hipLaunchKernelGGL(k_combine_bwd, dim3(cdiv(T, 4)), dim3(256), 0, s, dy, o, gates, topk_idx, row_of, T,
-                       H, E, k, d_o, dg, dz);
+    MOE_SLOT_DISPATCH(k_combine_bwd, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k, d_o,
+                      dg, dz_slot, dz);
   }
   return hipGetLastError();
 }

@@ -58,19 +58,20 @@ hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, in
 // y[t] = sum_j gates[t,j] o[row_of[t,j]] (0 for masked tokens).
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s);
-// dO[row_of[t,j]] = g dY[t]; dg = <dY[t], O[row]>; dz[t,:] (bf16, dense over E).
+// dO[row_of[t,j]] = g dY[t]; dg = <dY[t], O[row]>; dz per slot (fp32 [T,k])
+// and dense over E (bf16 [T,E]).
 hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
                               const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, bf16_t* dz, hipStream_t s);
+                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz, hipStream_t s);
 
 // ---- router backward (router_bwd.hip)
 int dwr_splits(int T);
 // dW_r = x^T dz via `dwr_splits(T)` fp32 partials in ws_f32 ([splits][H][E]).
 hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, float* ws_f32,
                       void* dw_r, bool f32_out, hipStream_t s);
-// dX[t] = sum_j dXp[row_of[t,j]] + dz[t] W_r^T.
-hipError_t launch_router_dx(const bf16_t* dz, const bf16_t* w_r, const bf16_t* dxp,
-                            const int32_t* row_of, int T, int H, int E, int k, bf16_t* dx,
-                            hipStream_t s);
+// dX[t] = sum_j (dXp[row_of[t,j]] + dz_j W_r[:, idx_j]); w_rt is [E,H] scratch.
+hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
+                            const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
+                            bf16_t* w_rt, bf16_t* dx, hipStream_t s);
 
 }  // namespace moe

@@ -121,8 +121,8 @@ size_t fwd_ws(const moe_dims* d) { return up(permute_ws_ints(d->T, d->E) * sizeo
 // ---- layout of the backward workspace
 struct BwdWs {
   bf16_t* d_o;  // also dXp once dO is dead
-  bf16_t *dg, *du, *dz;
-  float *dgate, *dwr_part;
+  bf16_t *dg, *du, *dz, *w_rt;
+  float *dgate, *dz_slot, *dwr_part;
   size_t bytes;
 };
 
@@ -135,6 +135,8 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
   w.du = c.take<bf16_t>(R * F);
   w.dz = c.take<bf16_t>(T * E);
   w.dgate = c.take<float>(T * k);
+  w.dz_slot = c.take<float>(T * k);
+  w.w_rt = c.take<bf16_t>(E * H);
   w.dwr_part = c.take<float>(static_cast<size_t>(dwr_splits(d->T)) * H * E);
   w.bytes = c.off;
   return w;
@@ -263,7 +265,7 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bool f32 = d->flags & MOE_F_DW_FP32;
   hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
-                                    T, H, E, k, w.d_o, w.dgate, w.dz, s);
+                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, s);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
@@ -272,8 +274,8 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   if (e != hipSuccess) return hip_status(e, "experts bwd");
   e = launch_dwr(static_cast<const bf16_t*>(x), w.dz, T, H, E, w.dwr_part, dw_r, f32, s);
   if (e != hipSuccess) return hip_status(e, "router weight grad");
-  e = launch_router_dx(w.dz, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
-                       static_cast<bf16_t*>(dx), s);
+  e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
+                       w.w_rt, static_cast<bf16_t*>(dx), s);
   return hip_status(e, "dx");
 }
 

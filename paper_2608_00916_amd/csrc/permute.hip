@@ -125,20 +125,27 @@ __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restri
   }
 }
 
-// xp[r] = x[row_token[r]] for r < offsets[E]; 16 bytes per thread.
+// xp[r] = x[row_token[r]] for r < offsets[E]: one wave per row, 16 bytes per
+// lane per pass, four passes' loads issued before their stores.
 __global__ __launch_bounds__(256) void k_gather(const bf16_t* __restrict__ x,
                                                 const int32_t* __restrict__ row_token,
                                                 const int32_t* __restrict__ offsets, int E, int H,
                                                 bf16_t* __restrict__ xp) {
   const int64_t R = offsets[E];
-  const int cpr = H / 8;  // 16-byte chunks per row
-  const int64_t n = R * cpr;
-  for (int64_t q = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; q < n;
-       q += static_cast<int64_t>(gridDim.x) * 256) {
-    const int64_t r = q / cpr;
-    const int c = static_cast<int>(q - r * cpr);
-    const int64_t t = row_token[r];
-    *reinterpret_cast<uint4*>(xp + r * H + c * 8) = *reinterpret_cast<const uint4*>(x + t * H + c * 8);
+  const int lane = threadIdx.x & 63;
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * 4;
+  for (int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); r < R; r += nwaves) {
+    const bf16_t* src = x + static_cast<int64_t>(row_token[r]) * H;
+    bf16_t* dst = xp + r * H;
+    int c = lane * 8;
+    for (; c + 3 * 512 < H; c += 4 * 512) {
+      uint4 v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = *reinterpret_cast<const uint4*>(src + c + i * 512);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(dst + c + i * 512) = v[i];
+    }
+    for (; c < H; c += 512) *reinterpret_cast<uint4*>(dst + c) = *reinterpret_cast<const uint4*>(src + c);
   }
 }
 
@@ -189,8 +196,7 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
     hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
                        row_token, row_of);
   }
-  const int64_t work = static_cast<int64_t>(T) * k * (H / 8);
-  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(work, 256), 4096));
+  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(static_cast<int64_t>(T) * k, 4), 8192));
   {
     TraceScope trace_scope(K_GATHER, s);
     hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, x, row_token, offsets, E, H, xp);

@@ -1,7 +1,7 @@
 // Router backward of the MoE block: dW_r = x^T dz (split over tokens into
 // fp32 partials reduced in a fixed order) and dX = (sum of the permuted-row
-// gradients of the token) + dz W_r^T, the latter a K = E MFMA product whose
-// epilogue gathers the token's rows.
+// gradients of the token) + dz W_r^T, where dz has only the k selected
+// experts non-zero, so its product with W_r^T is k scaled rows of W_r^T.
 #include <algorithm>
 
 #include "gemm_core.hpp"
@@ -59,46 +59,66 @@ __global__ __launch_bounds__(256) void k_dwr_reduce(const float* __restrict__ pa
   }
 }
 
-// dX[t][h] = sum_j dXp[row_of[t,j]][h] + sum_e dz[t][e] W_r[h][e];
-// tile 128 tokens x 128 hidden, K = E.
-__global__ __launch_bounds__(RTile::kThreads) void k_router_dx(const bf16_t* __restrict__ dz,
-                                                        const bf16_t* __restrict__ w_r,
-                                                        const bf16_t* __restrict__ dxp,
-                                                        const int32_t* __restrict__ row_of, int T, int H,
-                                                        int E, int k, bf16_t* __restrict__ dx) {
-  using C = RTile;
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
-  f32x4 acc[C::FM][C::FN];
-  zero_acc<C>(acc);
-  // B(k = e, n = h) = W_r[h][e]: K-contiguous rows of W_r.
-  const bf16_t* bs[1] = {w_r + static_cast<int64_t>(n0) * E};
-  gemm_mainloop<C, true, true>(dz + static_cast<int64_t>(m0) * E, E, min(C::BM, T - m0), bs, E, H - n0, E,
-                               smem, acc);
+// W_rT[E][H] = W_r[H][E] through 64 x 64 LDS tiles.
+__global__ __launch_bounds__(256) void k_transpose_wr(const bf16_t* __restrict__ w_r, int H, int E,
+                                                      bf16_t* __restrict__ w_rt) {
+  __shared__ bf16_t tile[64][65];
+  const int h0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int hh = i / 64, ee = i % 64;
+    if (h0 + hh < H && e0 + ee < E) tile[hh][ee] = w_r[static_cast<int64_t>(h0 + hh) * E + e0 + ee];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+    const int ee = i / 64, hh = i % 64;
+    if (h0 + hh < H && e0 + ee < E) w_rt[static_cast<int64_t>(e0 + ee) * H + h0 + hh] = tile[hh][ee];
+  }
+}
+
+// dX[t] = sum_j ( dXp[row_of[t,j]] + dz_j W_r[:, idx_j] ): dz is non-zero on
+// the k selected experts only, so the router term is k scaled rows of W_r^T
+// (L2-resident).  One wave per token, 8 columns per lane per pass.
+template <int KT>
+__global__ __launch_bounds__(256) void k_router_dx(const float* __restrict__ dz_slot,
+                                                   const int32_t* __restrict__ topk_idx,
+                                                   const bf16_t* __restrict__ w_rt,
+                                                   const bf16_t* __restrict__ dxp,
+                                                   const int32_t* __restrict__ row_of, int T, int H, int k,
+                                                   bf16_t* __restrict__ dx) {
   const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  int rows[KT], ex[KT];
+  float dzs[KT];
 #pragma unroll
-  for (int mi = 0; mi < C::FM; ++mi) {
-    const int t = m0 + frag_row<C>(mi, lane);
-    if (t >= T) continue;
-    const int32_t* rows = row_of + static_cast<int64_t>(t) * k;
+  for (int j = 0; j < KT; ++j) {
+    const int64_t p = static_cast<int64_t>(t) * k + j;
+    rows[j] = j < k ? row_of[p] : -1;
+    ex[j] = j < k ? topk_idx[p] : -1;
+    dzs[j] = j < k ? dz_slot[p] : 0.0f;
+  }
+  for (int c = lane * 8; c < H; c += kWave * 8) {
+    uint4 v[KT], w[KT];
 #pragma unroll
-    for (int ni = 0; ni < C::FN; ++ni) {
-      const int h = n0 + frag_col<C>(ni, lane);
-      float s[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < k; ++j) {
-        const int r = rows[j];
-        if (r < 0) continue;
-        const uint2 w = *reinterpret_cast<const uint2*>(dxp + static_cast<int64_t>(r) * H + h);
-        s[0] += lo_bf(w.x);
-        s[1] += hi_bf(w.x);
-        s[2] += lo_bf(w.y);
-        s[3] += hi_bf(w.y);
-      }
-      f32x4 v = acc[mi][ni];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] += s[i];
-      *reinterpret_cast<uint2*>(dx + static_cast<int64_t>(t) * H + h) = pack4_bf16(v);
+    for (int j = 0; j < KT; ++j) {
+      const bool on = rows[j] >= 0;
+      v[j] = on ? *reinterpret_cast<const uint4*>(dxp + static_cast<int64_t>(rows[j]) * H + c) : make_uint4(0, 0, 0, 0);
+      w[j] = on ? *reinterpret_cast<const uint4*>(w_rt + static_cast<int64_t>(ex[j]) * H + c) : make_uint4(0, 0, 0, 0);
     }
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      const uint32_t* pv = reinterpret_cast<const uint32_t*>(&v[j]);
+      const uint32_t* pw = reinterpret_cast<const uint32_t*>(&w[j]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += lo_bf(pv[q]) + dzs[j] * lo_bf(pw[q]);
+        acc[2 * q + 1] += hi_bf(pv[q]) + dzs[j] * hi_bf(pw[q]);
+      }
+    }
+    *reinterpret_cast<uint4*>(dx + static_cast<int64_t>(t) * H + c) =
+        make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                   pack_bf16x2(acc[6], acc[7]));
   }
 }
 
@@ -126,13 +146,22 @@ hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, fl
   return hipGetLastError();
 }
 
-hipError_t launch_router_dx(const bf16_t* dz, const bf16_t* w_r, const bf16_t* dxp,
-                            const int32_t* row_of, int T, int H, int E, int k, bf16_t* dx,
-                            hipStream_t s) {
+hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
+                            const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
+                            bf16_t* w_rt, bf16_t* dx, hipStream_t s) {
+  {
+    TraceScope trace_scope(K_TRANSPOSE_WR, s);
+    hipLaunchKernelGGL(k_transpose_wr, dim3(cdiv(H, 64), cdiv(E, 64)), dim3(256), 0, s, w_r, H, E, w_rt);
+  }
   {
     TraceScope trace_scope(K_ROUTER_DX, s);
-    hipLaunchKernelGGL(k_router_dx, dim3(cdiv(T, RTile::BM), H / RTile::BN), dim3(RTile::kThreads), 0, s, dz, w_r, dxp, row_of, T,
-                       H, E, k, dx);
+    const dim3 grid(cdiv(T, 4));
+    if (k <= 1) hipLaunchKernelGGL(k_router_dx<1>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    else if (k <= 2) hipLaunchKernelGGL(k_router_dx<2>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    else if (k <= 4) hipLaunchKernelGGL(k_router_dx<4>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    else if (k <= 8) hipLaunchKernelGGL(k_router_dx<8>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    else if (k <= 16) hipLaunchKernelGGL(k_router_dx<16>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    else hipLaunchKernelGGL(k_router_dx<32>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
   }
   return hipGetLastError();
 }

@@ -27,6 +27,7 @@ enum KernelId {
   K_DWR_REDUCE,
   K_ROUTER_DX,
   K_OFFSETS,
+  K_TRANSPOSE_WR,
   K_NUM_KERNELS
 };
 
