@@ -200,77 +200,106 @@ __device__ __forceinline__ void store4(void* out, int64_t idx, const f32x4& v) {
     *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out) + idx) = pack4_bf16(v);
 }
 
-// Weight-gradient tile: expert e, rows [m0, m0+BM), columns [n0, n0+BNS) of
-// each of the NB gradients (M x N each).
-struct WTile {
-  int e, m0, n0;
-};
+// Weight-gradient jobs: expert e, rows [m0, m0+BM), columns [n0, n0+BNS) of
+// each of the NB gradients (M x N each), K = rows of the expert (0 rows:
+// the tile is written as zeros).  Workgroup job i is logical tile
+// xcd_tile(block) + i * gridDim of E x (M/BM) x (N/BNS).
 template <class C>
-__device__ __forceinline__ WTile wgrad_tile(int M, int N) {
-  const int logical = xcd_tile(blockIdx.x, gridDim.x);
+__device__ __forceinline__ bool wgrad_locate(int i, int E, int M, int N, int& e, int& m0, int& n0) {
   const int nm = M / C::BM, nn = N / C::BNS;
-  WTile t;
-  t.e = logical / (nm * nn);
-  const int rem = logical - t.e * nm * nn;
-  t.m0 = (rem / nn) * C::BM;
-  t.n0 = (rem % nn) * C::BNS;
-  return t;
+  const int logical = xcd_tile(blockIdx.x, gridDim.x) + i * gridDim.x;
+  if (logical >= E * nm * nn) return false;
+  e = logical / (nm * nn);
+  const int rem = logical - e * nm * nn;
+  m0 = (rem / nn) * C::BM;
+  n0 = (rem % nn) * C::BNS;
+  return true;
 }
 
-// dW_down[e] (F x H) = A_e^T dO_e, K = rows of expert e.
-template <class C, bool F32>
-__global__ __launch_bounds__(C::kThreads) void k_down_wgrad(const bf16_t* __restrict__ act,
-                                                         const bf16_t* __restrict__ d_o,
-                                                         const int32_t* __restrict__ offsets, int E,
-                                                         int H, int F, void* __restrict__ dw_down) {
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  const WTile t = wgrad_tile<C>(F, H);
-  if (t.e >= E) return;
-  const int r0 = offsets[t.e], n_rows = offsets[t.e + 1] - r0;
-  f32x4 acc[C::FM][C::FN];
-  zero_acc<C>(acc);
-  const bf16_t* bs[1] = {d_o + static_cast<int64_t>(r0) * H + t.n0};
-  gemm_mainloop<C, false, false>(act + static_cast<int64_t>(r0) * F + t.m0, F, C::BM, bs, H, C::BN,
-                                 n_rows, smem, acc);
-  const int lane = threadIdx.x & 63;
-  const int64_t obase = static_cast<int64_t>(t.e) * F * H;
-#pragma unroll
-  for (int mi = 0; mi < C::FM; ++mi) {
-    const int64_t row = obase + static_cast<int64_t>(t.m0 + frag_row<C>(mi, lane)) * H + t.n0;
-#pragma unroll
-    for (int ni = 0; ni < C::FN; ++ni) store4<F32>(dw_down, row + frag_col<C>(ni, lane), acc[mi][ni]);
+// dW_down[e] (F x H) = A_e^T dO_e.
+template <class C_, bool F32>
+struct DownWgradJobs {
+  using C = C_;
+  const int32_t* offsets;
+  const bf16_t *act, *d_o;
+  int E, H, F;
+  void* dw_down;
+  __device__ bool get(int i, Job<C>& j) const {
+    int e, m0, n0;
+    if (!wgrad_locate<C>(i, E, F, H, e, m0, n0)) return false;
+    const int r0 = offsets[e];
+    j.a = act + static_cast<int64_t>(r0) * F + m0;
+    j.lda = F;
+    j.m_lim = C::BM;
+    j.b[0] = d_o + static_cast<int64_t>(r0) * H + n0;
+    j.ldb = H;
+    j.n_lim = C::BN;
+    j.K = offsets[e + 1] - r0;
+    j.chain = false;
+    j.e = e;
+    j.m0 = m0;
+    j.n0 = n0;
+    return true;
   }
-}
-
-// dW_gate[e] = Xp_e^T dG_e, dW_up[e] = Xp_e^T dU_e  (H x F each, K = rows).
-template <class C, bool F32>
-__global__ __launch_bounds__(C::kThreads) void k_gateup_wgrad(const bf16_t* __restrict__ xp,
-                                                           const bf16_t* __restrict__ dg_in,
-                                                           const bf16_t* __restrict__ du_in,
-                                                           const int32_t* __restrict__ offsets, int E,
-                                                           int H, int F, void* __restrict__ dw_gate,
-                                                           void* __restrict__ dw_up) {
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  const WTile t = wgrad_tile<C>(H, F);
-  if (t.e >= E) return;
-  const int r0 = offsets[t.e], n_rows = offsets[t.e + 1] - r0;
-  f32x4 acc[C::FM][C::FN];
-  zero_acc<C>(acc);
-  const int64_t bofs = static_cast<int64_t>(r0) * F + t.n0;
-  const bf16_t* bs[2] = {dg_in + bofs, du_in + bofs};
-  gemm_mainloop<C, false, false>(xp + static_cast<int64_t>(r0) * H + t.m0, H, C::BM, bs, F, C::BNS,
-                                 n_rows, smem, acc);
-  const int lane = threadIdx.x & 63;
-  const int64_t obase = static_cast<int64_t>(t.e) * H * F;
+  __device__ void epilogue(const Job<C>& j, f32x4 (&acc)[C::FM][C::FN]) const {
+    const int lane = threadIdx.x & 63;
+    const int64_t obase = static_cast<int64_t>(j.e) * F * H;
 #pragma unroll
-  for (int mi = 0; mi < C::FM; ++mi) {
-    const int64_t row = obase + static_cast<int64_t>(t.m0 + frag_row<C>(mi, lane)) * F + t.n0;
+    for (int mi = 0; mi < C::FM; ++mi) {
+      const int64_t row = obase + static_cast<int64_t>(j.m0 + frag_row<C>(mi, lane)) * H + j.n0;
 #pragma unroll
-    for (int ni = 0; ni < C::FN / 2; ++ni) {
-      store4<F32>(dw_gate, row + frag_col<C>(ni, lane), acc[mi][ni]);
-      store4<F32>(dw_up, row + frag_col<C>(ni, lane), acc[mi][ni + C::FN / 2]);
+      for (int ni = 0; ni < C::FN; ++ni) store4<F32>(dw_down, row + frag_col<C>(ni, lane), acc[mi][ni]);
     }
   }
+};
+
+// dW_gate[e] = Xp_e^T dG_e, dW_up[e] = Xp_e^T dU_e  (H x F each).
+template <class C_, bool F32>
+struct GateUpWgradJobs {
+  using C = C_;
+  const int32_t* offsets;
+  const bf16_t *xp, *dg_in, *du_in;
+  int E, H, F;
+  void *dw_gate, *dw_up;
+  __device__ bool get(int i, Job<C>& j) const {
+    int e, m0, n0;
+    if (!wgrad_locate<C>(i, E, H, F, e, m0, n0)) return false;
+    const int r0 = offsets[e];
+    const int64_t bofs = static_cast<int64_t>(r0) * F + n0;
+    j.a = xp + static_cast<int64_t>(r0) * H + m0;
+    j.lda = H;
+    j.m_lim = C::BM;
+    j.b[0] = dg_in + bofs;
+    j.b[1] = du_in + bofs;
+    j.ldb = F;
+    j.n_lim = C::BNS;
+    j.K = offsets[e + 1] - r0;
+    j.chain = false;
+    j.e = e;
+    j.m0 = m0;
+    j.n0 = n0;
+    return true;
+  }
+  __device__ void epilogue(const Job<C>& j, f32x4 (&acc)[C::FM][C::FN]) const {
+    const int lane = threadIdx.x & 63;
+    const int64_t obase = static_cast<int64_t>(j.e) * H * F;
+#pragma unroll
+    for (int mi = 0; mi < C::FM; ++mi) {
+      const int64_t row = obase + static_cast<int64_t>(j.m0 + frag_row<C>(mi, lane)) * F + j.n0;
+#pragma unroll
+      for (int ni = 0; ni < C::FN / 2; ++ni) {
+        store4<F32>(dw_gate, row + frag_col<C>(ni, lane), acc[mi][ni]);
+        store4<F32>(dw_up, row + frag_col<C>(ni, lane), acc[mi][ni + C::FN / 2]);
+      }
+    }
+  }
+};
+
+// One persistent kernel for every product: the job provider decides.
+template <class P, bool A_KC, bool B_KC>
+__global__ __launch_bounds__(P::C::kThreads) void k_stream(P prov) {
+  __shared__ __attribute__((aligned(16))) char smem[P::C::kLds];
+  gemm_stream<typename P::C, A_KC, B_KC>(prov, smem);
 }
 
 inline int grid8(int64_t n) { return static_cast<int>(cdiv64(n, 8) * 8); }
@@ -310,24 +339,28 @@ int persistent_grid(Kernel kernel, int threads, int64_t max_tiles) {
 // Upper bound of the number of 128-row tiles over all experts.
 int max_row_tiles(int rows_cap, int E) { return cdiv(rows_cap, kRowTile) + E; }
 
-hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s) {
-  using C = GateUpFwd;
-  const int grid =
-      persistent_grid(k_gateup_fwd, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
-  {
-    TraceScope trace_scope(K_GATEUP_FWD, s);
-    hipLaunchKernelGGL(k_gateup_fwd, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.w_gate, a.w_up, a.offsets,
-                       a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
-  }
-  return hipGetLastError();
-}
-
 namespace {
+
+// Tile shapes: 128 rows x 256 columns over 8 waves (2 x 4, 64 x 64 each, two
+// waves per SIMD so one's MFMAs cover the other's LDS waits); 128 x 128 over
+// 4 waves when a dimension is not a multiple of 256.
+using Wide = Tile<128, 256, 1, 2, 4>;
+using Narrow = Tile<128, 128, 1, 2, 2>;
+using WideGU = Tile<128, 256, 2, 2, 4>;
+
+template <bool A_KC, bool B_KC, class P>
+void run_stream(const P& prov, int64_t max_jobs, int kid, hipStream_t s) {
+  auto k = k_stream<P, A_KC, B_KC>;
+  const int grid = persistent_grid(k, P::C::kThreads, max_jobs);
+  TraceScope trace_scope(kid, s);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(P::C::kThreads), 0, s, prov);
+}
 
 template <class C>
 void down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   auto k = k_down_fwd<C>;
-  const int grid = persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
+  const int grid =
+      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_DOWN_FWD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.act, a.w_down, a.offsets, a.tile_start, a.E,
                      a.H, a.F, o);
@@ -336,7 +369,8 @@ void down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
 template <class C>
 void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, hipStream_t s) {
   auto k = k_down_dgrad_swiglu<C>;
-  const int grid = persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN));
+  const int grid =
+      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN));
   TraceScope trace_scope(K_DOWN_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start,
                      a.E, a.H, a.F, dg, du);
@@ -345,7 +379,8 @@ void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, 
 template <class C>
 void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp, hipStream_t s) {
   auto k = k_gateup_dgrad<C>;
-  const int grid = persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
+  const int grid =
+      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_GATEUP_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start,
                      a.E, a.H, a.F, dxp);
@@ -353,19 +388,15 @@ void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_
 
 template <class C, bool F32>
 void down_wgrad(const ExpertArgs& a, const bf16_t* d_o, void* dw_down, hipStream_t s) {
-  const int grid = grid8(static_cast<int64_t>(a.E) * (a.F / C::BM) * (a.H / C::BNS));
-  TraceScope trace_scope(K_DOWN_WGRAD, s);
-  hipLaunchKernelGGL((k_down_wgrad<C, F32>), dim3(grid), dim3(C::kThreads), 0, s, a.act, d_o, a.offsets, a.E,
-                     a.H, a.F, dw_down);
+  DownWgradJobs<C, F32> p{a.offsets, a.act, d_o, a.E, a.H, a.F, dw_down};
+  run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.F / C::BM) * (a.H / C::BNS), K_DOWN_WGRAD, s);
 }
 
 template <class C, bool F32>
 void gateup_wgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate, void* dw_up,
                   hipStream_t s) {
-  const int grid = grid8(static_cast<int64_t>(a.E) * (a.H / C::BM) * (a.F / C::BNS));
-  TraceScope trace_scope(K_GATEUP_WGRAD, s);
-  hipLaunchKernelGGL((k_gateup_wgrad<C, F32>), dim3(grid), dim3(C::kThreads), 0, s, a.xp, dg, du, a.offsets,
-                     a.E, a.H, a.F, dw_gate, dw_up);
+  GateUpWgradJobs<C, F32> p{a.offsets, a.xp, dg, du, a.E, a.H, a.F, dw_gate, dw_up};
+  run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.H / C::BM) * (a.F / C::BNS), K_GATEUP_WGRAD, s);
 }
 
 template <class C>
@@ -383,12 +414,17 @@ void gateup_wgrad_any(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, v
 
 }  // namespace
 
-// Tile shapes: 128 rows x 256 columns over 8 waves (2 x 4, 64 x 64 each, two
-// waves per SIMD so one's MFMAs cover the other's LDS waits); 128 x 128 over
-// 4 waves when a dimension is not a multiple of 256.
-using Wide = Tile<128, 256, 1, 2, 4>;
-using Narrow = Tile<128, 128, 1, 2, 2>;
-using WideGU = Tile<128, 256, 2, 2, 4>;
+hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s) {
+  using C = GateUpFwd;
+  const int grid = persistent_grid(k_gateup_fwd, C::kThreads,
+                                   static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
+  {
+    TraceScope trace_scope(K_GATEUP_FWD, s);
+    hipLaunchKernelGGL(k_gateup_fwd, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.w_gate, a.w_up, a.offsets,
+                       a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   if (a.H % 256 == 0) down_fwd<Wide>(a, o, s);

@@ -101,6 +101,7 @@ struct LoadKc {
       off[i] = static_cast<uint32_t>((q >> 3) * ld2 + ((q & 7) << 4));
     }
   }
+  __device__ __forceinline__ void disable() { valid = 0; }
   __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int K, int tid) const {
     const int64_t step = static_cast<int64_t>(kt) * (BK * 2);
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base + step, valid - step);
@@ -143,6 +144,7 @@ struct LoadMn {
       off[i] = u * 8 < r_lim ? static_cast<uint32_t>(k * ld2 + u * 16) : kOob;
     }
   }
+  __device__ __forceinline__ void disable() { valid = 0; }
   __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int, int) const {
     const int64_t step = static_cast<int64_t>(kt) * BK * ld2;
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base + step, valid - step);
@@ -237,6 +239,21 @@ __device__ __forceinline__ void zero_acc(f32x4 (&acc)[C::FM][C::FN]) {
   for (int mi = 0; mi < C::FM; ++mi)
 #pragma unroll
     for (int ni = 0; ni < C::FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Scheduling: each of the N MFMAs of a region is followed by an even share
+// of A instructions of class MA and B instructions of class MB.
+__host__ __device__ constexpr int share(int total, int slots, int i) {
+  return total * (i + 1) / slots - total * i / slots;
+}
+template <int N, int A, int MA, int B, int MB, int I = 0>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < N) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (share(A, N, I) > 0) __builtin_amdgcn_sched_group_barrier(MA, share(A, N, I), 0);
+    if constexpr (share(B, N, I) > 0) __builtin_amdgcn_sched_group_barrier(MB, share(B, N, I), 0);
+    interleave<N, A, MA, B, MB, I + 1>();
+  }
 }
 
 // acc += A(0:BM, 0:K) * [B_0 | B_1](0:K, 0:BN).
@@ -335,6 +352,154 @@ __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int 
     step(S0{}, kt);
     if (kt + 1 < nk) step(S1{}, kt + 1);
   }
+}
+
+// ---------------------------------------------------------------- persistent stream
+// A workgroup's sequence of tile jobs.  A job is one tile's K range of one
+// product; `chain` jobs accumulate into the next job's tile (a K range split
+// over two operand pairs) instead of ending it.
+template <class C>
+struct Job {
+  const bf16_t* a;
+  int64_t lda;
+  int m_lim;
+  const bf16_t* b[C::NB];
+  int64_t ldb;
+  int n_lim;
+  int K;       // valid k; 0 = an empty tile (its epilogue sees zeros)
+  bool chain;  // the next job continues this tile
+  int e, m0, n0;
+};
+
+// Runs every job of this workgroup (P::get(i, job) fills the i-th, false past
+// the end; P::epilogue(job, acc) consumes a finished tile) as one continuous
+// pipeline over the K steps of all jobs: the loads of step s + 3 and the LDS
+// writes of step s + 1 overlap the MFMAs of step s even across tile
+// boundaries, so a tile's first loads are in flight during the previous
+// tile's last steps and its epilogue.
+template <class C, bool A_KC, bool B_KC, class P>
+__device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
+  using LA = Loader<A_KC, C::BM, C::BM, C::kThreads>;
+  using LB = Loader<B_KC, C::BNS, C::BN, C::kThreads>;
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  LA la;
+  LB lb[C::NB];
+  uint4 ra[2][LA::kPer];
+  uint4 rb[2][C::NB][LB::kPer];
+  f32x4 acc[C::FM][C::FN];
+  zero_acc<C>(acc);
+
+  // load cursor: job li, step lkt.  Loads are issued unconditionally; once the
+  // cursor has run past the last job the loaders read zeros without touching
+  // memory.
+  int li = 0, lkt = 0;
+  Job<C> lj;
+  bool lok = prov.get(0, lj);
+  auto lsettle = [&]() {  // skip empty jobs, then set the loaders up for lj
+    while (lok && lj.K <= 0) lok = prov.get(++li, lj);
+    if (lok) {
+      la.setup(lj.a, lj.lda, lj.m_lim, lj.K, tid);
+#pragma unroll
+      for (int i = 0; i < C::NB; ++i) lb[i].setup(lj.b[i], lj.ldb, lj.n_lim, lj.K, tid);
+    } else {
+      la.disable();
+#pragma unroll
+      for (int i = 0; i < C::NB; ++i) lb[i].disable();
+    }
+  };
+  lsettle();
+  auto load = [&](auto set) {
+    constexpr int S = decltype(set)::value;
+    la.load(ra[S], lkt, lj.K, tid);
+#pragma unroll
+    for (int i = 0; i < C::NB; ++i) lb[i].load(rb[S][i], lkt, lj.K, tid);
+  };
+  auto lnext = [&]() {
+    if (lok && ++lkt * BK >= lj.K) {
+      lkt = 0;
+      lok = prov.get(++li, lj);
+      lsettle();
+    }
+  };
+  auto store = [&](auto set, char* stage) {
+    constexpr int S = decltype(set)::value;
+    la.store(ra[S], stage, 0, tid);
+#pragma unroll
+    for (int i = 0; i < C::NB; ++i) lb[i].store(rb[S][i], stage + C::kABytes, i * C::BNS, tid);
+  };
+
+  // compute cursor: job ci, step ckt
+  int ci = 0, ckt = 0;
+  Job<C> cj;
+  bool cok = prov.get(0, cj);
+  auto csettle = [&]() {  // finish empty jobs (their tiles are zero unless chained)
+    while (cok && cj.K <= 0) {
+      if (!cj.chain) {
+        prov.epilogue(cj, acc);
+        zero_acc<C>(acc);
+      }
+      cok = prov.get(++ci, cj);
+    }
+  };
+  csettle();
+  auto cadvance = [&]() {
+    if (++ckt * BK >= cj.K) {
+      ckt = 0;
+      if (!cj.chain) {
+        prov.epilogue(cj, acc);
+        zero_acc<C>(acc);
+      }
+      cok = prov.get(++ci, cj);
+      csettle();
+    }
+  };
+
+  constexpr int kReads = C::FM * (A_KC ? 1 : 2) + C::FN * (B_KC ? 1 : 2);
+  constexpr int kMfma = C::FM * C::FN;
+  constexpr int kWrites = LA::kPer + C::NB * LB::kPer;
+  constexpr int kLoads = kWrites;
+  static_assert(kReads <= kMfma, "slice reads must fit between the MFMAs of a slice");
+  static_assert(kWrites + kLoads <= kMfma, "refill must fit between the MFMAs of a slice");
+  auto step = [&](auto set) {
+    constexpr int S = decltype(set)::value;
+    using Other = std::integral_constant<int, 1 - S>;
+    const char* cur = smem + S * C::kStage;
+    char* nxt = smem + (1 - S) * C::kStage;
+    uint4 af0[C::FM], bf0[C::FN], af1[C::FM], bf1[C::FN];
+    read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 0, lane, af0, bf0);
+    read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 1, lane, af1, bf1);
+    mfmas<C>(af0, bf0, acc);
+    mfmas<C>(af1, bf1, acc);
+    store(Other{}, nxt);
+    load(Other{});
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+    interleave<kMfma, kReads, 0x100, 0, 0x200>();
+    interleave<kMfma, kWrites, 0x200, kLoads, 0x020>();
+    lds_barrier();
+    lnext();
+  };
+
+  if (!cok) return;
+  load(S0{});
+  lnext();
+  load(S1{});
+  lnext();
+  store(S0{}, smem);
+  lds_barrier();
+  load(S0{});
+  lnext();
+  while (cok) {
+    step(S0{});
+    cadvance();
+    if (!cok) break;
+    step(S1{});
+    cadvance();
+  }
+  lds_barrier();  // the workgroup's LDS is free again
 }
 
 // Output coordinates of fragment (mi, ni) for this lane: row, first of 4 columns
