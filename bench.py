@@ -16,8 +16,12 @@ sample of the same workload, timed on this host's cores.
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -26,6 +30,10 @@ import numpy as np
 import workloads
 
 METRIC = "MoE block fwd+bwd tokens/sec and TFLOP/s (% bf16 MFMA peak), 1 MI355X"
+ROOT = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(ROOT, "paper_2608_00916_amd", "csrc")
+TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic_{}.json")
+COPY_TAG = "copy calibration"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
@@ -48,6 +56,78 @@ def kernel_work(name, T, Tv, H, E, F, k, R):
         "combine": ("byte", float(R * H * b + Tv * H * b)),
         "combine_bwd": ("byte", float(Tv * H * b + 2 * R * H * b)),
     }.get(name, ("none", 0.0))
+
+
+def kernel_source_hash():
+    """sha256 over the kernel sources: stored counter readings apply only to
+    the kernels they were taken from."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(CSRC, "*"))):
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def short_kernel_name(name):
+    """rocprofv3 kernel name -> the library's trace name."""
+    m = re.search(r"k_stream<[^>]*?::(\w+)Jobs", name)
+    if m:
+        return {"DownWgrad": "down_wgrad", "GateUpWgrad": "gateup_wgrad"}.get(m.group(1), m.group(1))
+    m = re.search(r"k_(\w+?)(?:<|\(|$)", name)
+    if m:
+        return m.group(1)
+    return name[:40]
+
+
+def pmc_summary(fetch_dir, write_dir, workload, copy_mib):
+    """Turn two rocprofv3 --pmc runs of `bench.py --copy-calibration N` (one
+    with FETCH_SIZE, one with WRITE_SIZE, KiB per dispatch) into HBM bytes per
+    launch for each library kernel.  Each counter is scaled by the ratio of
+    the known bytes of the torch copy kernel (N MiB read, N MiB written) to
+    what the counter read for it."""
+    def read(d, counter):
+        rows = list(csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))))
+        per = {}
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return per
+    f = read(fetch_dir, "FETCH_SIZE")
+    w = read(write_dir, "WRITE_SIZE")
+    copy_bytes = copy_mib * 2 ** 20
+    # the calibration copy is the dispatch reading about copy_mib MiB outside the library
+    cands = [(n, max(v)) for n, v in f.items() if "moe::" not in n]
+    cname, cfetch = min(cands, key=lambda x: abs(x[1] * 1024 - copy_bytes))
+    cwrite = max(w[cname])
+    ff = copy_bytes / (cfetch * 1024)
+    wf = copy_bytes / (cwrite * 1024)
+    kernels = {}
+    for n, v in f.items():
+        if "moe::" not in n:
+            continue
+        kn = short_kernel_name(n)
+        fb = sum(v) / len(v) * 1024 * ff
+        wb = sum(w.get(n, [0.0])) / max(1, len(w.get(n, []))) * 1024 * wf
+        kernels[kn] = {"fetch_bytes": round(fb), "write_bytes": round(wb), "hbm_bytes": round(fb + wb)}
+    out = {"workload": workload, "source_hash": kernel_source_hash(), "copy_kernel": cname[:80],
+           "copy_bytes": copy_bytes, "fetch_factor": ff, "write_factor": wf, "kernels": kernels}
+    path = TRAFFIC.format(workload)
+    json.dump(out, open(path, "w"), indent=1)
+    print(f"wrote {path}: fetch x{ff:.3f}, write x{wf:.3f}")
+
+
+def stored_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the stored counter summary, or
+    None if there is none or the kernels changed since it was taken."""
+    try:
+        d = json.load(open(TRAFFIC.format(workload)))
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    k = d.get("kernels", {}).get(kernel)
+    return None if k is None else k["hbm_bytes"]
 
 
 def cpu_baseline(inp, k, tokens):
@@ -77,11 +157,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_30b_a3b",
                     choices=[n for n, c in workloads.CONFIGS.items() if c["kind"] == "block"])
-    ap.add_argument("--cpu-tokens", type=int, default=2048,
+    ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens of the oracle's CPU-baseline sample (0 = skip)")
     ap.add_argument("--no-trace", action="store_true",
                     help="do not record per-kernel events in the timed region")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="run one torch copy of MIB MiB before the steps (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc runs into profiles/ and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.workload, args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the block runs on a single MI355X and this build has "
               f"no multi-GPU path (--gpus {args.gpus} requested)", file=sys.stderr)
@@ -105,6 +192,14 @@ def main():
     t = {n: dev(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
     tm = None if mask_np is None else torch.from_numpy(mask_np.astype(np.uint8)).cuda()
     blk = moe.MoEBlock(T, H, E, F, k, mask=tm is not None)
+
+    if args.copy_calibration:
+        n = args.copy_calibration * 2 ** 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
@@ -175,14 +270,15 @@ def main():
         tot, n = kern[dom]
         avg_s = tot / n * 1e-3
         kind, amt = kernel_work(dom, T, Tv, H, E, F, k, R)
+        traffic = stored_traffic(args.workload, dom)
         if kind == "flop":
             ach = amt / avg_s / 1e12
             out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
-                               "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": None}
+                               "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic}
         else:
             ach = amt / avg_s / 1e9
             out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
-                               "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None}
+                               "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
     if args.cpu_tokens > 0:
         print(f"[bench] CPU baseline: oracle on {args.cpu_tokens} tokens", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(inp, k, min(args.cpu_tokens, T))
