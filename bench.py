@@ -150,11 +150,36 @@ def cpu_baseline(inp, k, tokens):
                       f"{dt:.1f} s"}
 
 
+def serving_forward(moe, t, tm, T, H, E, F, k, Tv, steps, warmup):
+    """The forward-only entry point (moe_infer) on the same batch, timed after
+    the fwd+bwd region: tokens/s of the serving pass."""
+    import torch
+    inf = moe.MoEInfer(T, H, E, F, k, mask=tm is not None)
+
+    def run():
+        inf.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+
+    for _ in range(warmup):
+        run()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(f"[bench] forward only (moe_infer): {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    return {"entry": "moe_infer", "tokens_per_s": Tv / (ms * 1e-3), "ms_per_step": ms, "steps": steps,
+            "tflops": 6.0 * H * F * Tv * k / (ms * 1e-3) / 1e12}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3_30b_a3b",
                     choices=[n for n, c in workloads.CONFIGS.items() if c["kind"] == "block"])
     ap.add_argument("--cpu-tokens", type=int, default=8192,
@@ -201,9 +226,15 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    def step():
+    def step(marks=None):
+        if marks:
+            marks[0].record()
         blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+        if marks:
+            marks[1].record()
         blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
+        if marks:
+            marks[2].record()
 
     for _ in range(args.warmup):
         step()
@@ -215,11 +246,12 @@ def main():
         moe.moe_trace_enable(True)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     ev0.record()
-    for _ in range(args.steps):
-        step()
+    for i in range(args.steps):
+        step(marks[i])
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -228,6 +260,14 @@ def main():
     kern = moe.moe_trace_read()
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})",
           file=sys.stderr, flush=True)
+
+    def pct(v):
+        q = np.percentile(np.asarray(v), [10, 50, 90])
+        return {"p10": round(float(q[0]), 4), "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4)}
+    timing = {"fwd_ms": pct([m[0].elapsed_time(m[1]) for m in marks]),
+              "bwd_ms": pct([m[1].elapsed_time(m[2]) for m in marks]),
+              "step_ms": pct([m[0].elapsed_time(m[2]) for m in marks])}
+    forward_only = serving_forward(moe, t, tm, T, H, E, F, k, Tv, args.steps, args.warmup)
 
     gemm_flop = 18.0 * H * F * R
     router_flop = 6.0 * H * E * Tv
@@ -249,6 +289,8 @@ def main():
                    "E": E, "top_k": k, "F": F, "routed_rows": R, "seed": cfg["seed"]},
         "block_tflops": tflops,
         "block_frac_bf16_peak": tflops / PEAK_BF16_TFLOPS,
+        "timing": timing,
+        "forward_only": forward_only,
     }
     if kern:
         per = {}

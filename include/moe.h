@@ -65,6 +65,11 @@ extern "C" {
 /* flags (moe_dims.flags, moe_experts_dims.flags) */
 #define MOE_F_MASK 1u    /* token_mask is given: tokens with mask 0 are not routed */
 #define MOE_F_DW_FP32 2u /* weight gradients (dW_r, dW_gate, dW_up, dW_down) are fp32, else bf16 */
+#define MOE_F_RECOMPUTE 4u /* the forward keeps no G and U (their saved views are NULL and the
+                            * saved buffer shrinks by 2 * R_cap * F * 2 bytes); the backward
+                            * recomputes them from Xp with the forward's own kernel, one more
+                            * gate/up product, so every output is bit-identical to a run
+                            * without the flag */
 
 /* Sizes of the full block.  T tokens (T >= 1), hidden size H, E experts,
  * expert width F, top_k experts per token. */
@@ -85,8 +90,8 @@ typedef struct moe_saved_view {
   int32_t* row_token; /* [R_cap]     token of row r for r < R, -1 beyond */
   int32_t* row_of;    /* [T, k]      row of (token, slot); -1 for masked tokens */
   void* xp;           /* [R_cap, H]  bf16 permuted tokens (rows >= R undefined) */
-  void* g;            /* [R_cap, F]  bf16 gate projection G */
-  void* u;            /* [R_cap, F]  bf16 up projection U */
+  void* g;            /* [R_cap, F]  bf16 gate projection G (NULL with MOE_F_RECOMPUTE) */
+  void* u;            /* [R_cap, F]  bf16 up projection U (NULL with MOE_F_RECOMPUTE) */
   void* a;            /* [R_cap, F]  bf16 SwiGLU activation A = silu(G) * U */
   void* o;            /* [R_cap, H]  bf16 expert outputs O (ungated) */
 } moe_saved_view;
@@ -131,19 +136,34 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
             void* dx, void* dw_r, void* dw_gate, void* dw_up, void* dw_down, void* ws,
             size_t ws_bytes, void* stream);
 
+/* Forward-only pass of the block for serving (reranking scores a batch of
+ * query-passage pairs in one prefill pass, §4.2 "Inference throughput"): the Y of
+ * moe_fwd, bit for bit, without a saved buffer.  Routing, A and O live in the
+ * workspace, G and U are never stored, and the gate/up product reads its rows
+ * of x through the permutation instead of a gathered copy (a copy is made in
+ * the workspace only when T * H * 2 bytes exceed 2^31 - 1).  MOE_F_MASK as in
+ * moe_fwd; MOE_F_DW_FP32 and MOE_F_RECOMPUTE are ignored.
+ *   x, w_r, w_gate, w_up, w_down, token_mask, y   as in moe_fwd
+ *   ws    moe_infer_workspace_bytes(d) bytes of scratch
+ */
+size_t moe_infer_workspace_bytes(const moe_dims* d);
+int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+              const void* w_up, const void* w_down, const uint8_t* token_mask, void* y,
+              void* ws, size_t ws_bytes, void* stream);
+
 /* One expert-parallel rank's share (§3, "Expert parallelism and topology"):
  * the rows dispatched to this rank's E local experts, already grouped
  * expert-major.  rows = capacity of the row buffers (rows >= 1). */
 typedef struct moe_experts_dims {
   int32_t rows, H, E, F;
-  uint32_t flags; /* MOE_F_DW_FP32 only */
+  uint32_t flags; /* MOE_F_DW_FP32, MOE_F_RECOMPUTE */
 } moe_experts_dims;
 
 /* Device pointers into an experts `saved` buffer. */
 typedef struct moe_experts_saved_view {
   int32_t* offsets; /* [E + 1] exclusive prefix sum of counts, clamped to rows */
-  void* g;          /* [rows, F] bf16 */
-  void* u;          /* [rows, F] bf16 */
+  void* g;          /* [rows, F] bf16 (NULL with MOE_F_RECOMPUTE) */
+  void* u;          /* [rows, F] bf16 (NULL with MOE_F_RECOMPUTE) */
   void* a;          /* [rows, F] bf16 */
 } moe_experts_saved_view;
 

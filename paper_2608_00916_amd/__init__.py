@@ -12,26 +12,30 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_MAX_EXPERTS, MOE_MAX_TOPK, MoeDims,
+from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_F_RECOMPUTE, MOE_MAX_EXPERTS, MOE_MAX_TOPK, MoeDims,
                    MoeError, MoeExpertsDims, MoeExpertsSavedView, MoeSavedView, check, lib)
 
 __all__ = [
     "dims", "experts_dims", "moe_saved_bytes", "moe_fwd_workspace_bytes",
     "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_bwd",
+    "moe_infer_workspace_bytes", "moe_infer", "MoEInfer",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes", "moe_experts_saved_views",
     "moe_experts_fwd", "moe_experts_bwd", "moe_last_error", "moe_version",
     "moe_trace_enable", "moe_trace_read", "MoEBlock", "MoEExperts", "MoeError", "MOE_F_MASK", "MOE_F_DW_FP32",
+    "MOE_F_RECOMPUTE",
     "MOE_MAX_EXPERTS", "MOE_MAX_TOPK",
 ]
 
 
-def dims(T, H, E, F, top_k, mask=False, dw_fp32=False) -> MoeDims:
-    flags = (MOE_F_MASK if mask else 0) | (MOE_F_DW_FP32 if dw_fp32 else 0)
+def dims(T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False) -> MoeDims:
+    flags = ((MOE_F_MASK if mask else 0) | (MOE_F_DW_FP32 if dw_fp32 else 0)
+             | (MOE_F_RECOMPUTE if recompute else 0))
     return MoeDims(T, H, E, F, top_k, flags)
 
 
-def experts_dims(rows, H, E, F, dw_fp32=False) -> MoeExpertsDims:
-    return MoeExpertsDims(rows, H, E, F, MOE_F_DW_FP32 if dw_fp32 else 0)
+def experts_dims(rows, H, E, F, dw_fp32=False, recompute=False) -> MoeExpertsDims:
+    return MoeExpertsDims(rows, H, E, F, (MOE_F_DW_FP32 if dw_fp32 else 0)
+                          | (MOE_F_RECOMPUTE if recompute else 0))
 
 
 def _p(t):
@@ -90,6 +94,8 @@ def moe_bwd_workspace_bytes(d: MoeDims) -> int:
 
 
 def _view(base: torch.Tensor, ptr: int, dtype, shape):
+    if ptr is None:  # a region the flags leave out
+        return None
     off = ptr - base.data_ptr()
     n = 1
     for s in shape:
@@ -134,6 +140,17 @@ def moe_bwd(d, x, w_r, w_gate, w_up, w_down, dy, saved, dx, dw_r, dw_gate, dw_up
                         0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
 
 
+# ------------------------------------------------------------------ forward only
+def moe_infer_workspace_bytes(d: MoeDims) -> int:
+    return lib().moe_infer_workspace_bytes(ctypes.byref(d))
+
+
+def moe_infer(d, x, w_r, w_gate, w_up, w_down, token_mask, y, ws, stream=None):
+    check(lib().moe_infer(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
+                          _p(token_mask), _p(y), _p(ws),
+                          0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
 # ------------------------------------------------------------------ experts only
 def moe_experts_saved_bytes(d: MoeExpertsDims) -> int:
     return lib().moe_experts_saved_bytes(ctypes.byref(d))
@@ -171,8 +188,8 @@ class MoEBlock:
     """Caller-side buffers for one block shape: saved activations, workspaces
     and outputs, allocated once with torch on `device`."""
 
-    def __init__(self, T, H, E, F, top_k, mask=False, dw_fp32=False, device="cuda"):
-        self.d = dims(T, H, E, F, top_k, mask, dw_fp32)
+    def __init__(self, T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False, device="cuda"):
+        self.d = dims(T, H, E, F, top_k, mask, dw_fp32, recompute)
         nb = moe_saved_bytes(self.d)
         if nb == 0:
             raise MoeError(_lib.MOE_ERR_ARG, moe_last_error())
@@ -202,8 +219,8 @@ class MoEBlock:
 class MoEExperts:
     """Caller-side buffers for one expert-parallel rank's local experts."""
 
-    def __init__(self, rows, H, E, F, dw_fp32=False, device="cuda"):
-        self.d = experts_dims(rows, H, E, F, dw_fp32)
+    def __init__(self, rows, H, E, F, dw_fp32=False, recompute=False, device="cuda"):
+        self.d = experts_dims(rows, H, E, F, dw_fp32, recompute)
         dev = torch.device(device)
         self.saved = torch.empty(moe_experts_saved_bytes(self.d), dtype=torch.uint8, device=dev)
         self.ws = torch.empty(moe_experts_workspace_bytes(self.d), dtype=torch.uint8, device=dev)
@@ -223,3 +240,21 @@ class MoEExperts:
         moe_experts_bwd(self.d, xp, w_gate, w_up, w_down, d_o, self.saved, self.dxp, self.dw_gate,
                         self.dw_up, self.dw_down, self.ws, stream)
         return self.dxp, self.dw_gate, self.dw_up, self.dw_down
+
+
+class MoEInfer:
+    """Caller-side buffers of the forward-only (serving) pass: workspace and
+    output for one block shape."""
+
+    def __init__(self, T, H, E, F, top_k, mask=False, device="cuda"):
+        self.d = dims(T, H, E, F, top_k, mask)
+        nb = moe_infer_workspace_bytes(self.d)
+        if nb == 0:
+            raise MoeError(_lib.MOE_ERR_ARG, moe_last_error())
+        dev = torch.device(device)
+        self.ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+
+    def forward(self, x, w_r, w_gate, w_up, w_down, token_mask=None, stream=None):
+        moe_infer(self.d, x, w_r, w_gate, w_up, w_down, token_mask, self.y, self.ws, stream)
+        return self.y

@@ -21,10 +21,11 @@ MOE_MAX_EXPERTS = 256
 MOE_MAX_TOPK = 32
 MOE_F_MASK = 1
 MOE_F_DW_FP32 = 2
+MOE_F_RECOMPUTE = 4
 
 EXPORTS = (
     "moe_saved_bytes", "moe_fwd_workspace_bytes", "moe_bwd_workspace_bytes",
-    "moe_saved_views", "moe_fwd", "moe_bwd",
+    "moe_saved_views", "moe_fwd", "moe_bwd", "moe_infer_workspace_bytes", "moe_infer",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes",
     "moe_experts_saved_views", "moe_experts_fwd", "moe_experts_bwd",
     "moe_trace_enable", "moe_trace_read", "moe_trace_name",
@@ -82,6 +83,8 @@ def lib() -> ctypes.CDLL:
         "moe_saved_views": (ctypes.c_int, [D, P, ctypes.POINTER(MoeSavedView)]),
         "moe_fwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, S, P]),
         "moe_bwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, P, P, P, P, S, P]),
+        "moe_infer_workspace_bytes": (S, [D]),
+        "moe_infer": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, S, P]),
         "moe_experts_saved_bytes": (S, [ED]),
         "moe_experts_workspace_bytes": (S, [ED]),
         "moe_experts_saved_views": (ctypes.c_int, [ED, P, ctypes.POINTER(MoeExpertsSavedView)]),

@@ -44,8 +44,14 @@ __device__ __forceinline__ void for_each_grouped_tile(const int32_t* offsets, co
 
 // G = Xp W_gate[e], U = Xp W_up[e], A = silu(G) * U  (K = H, N = F).
 // The B tile holds 128 columns of W_gate next to the same 128 of W_up.
+// G and U are stored when g_out is non-null, A when a_out is.  With xp_rows
+// non-null, row r of the product is row xp_rows[r] of xp (the gather read
+// through the permutation; xp_bytes bounds xp).
 using GateUpFwd = Tile<128, 256, 2, 2, 4>;
+template <bool kRows>
 __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t* __restrict__ xp,
+                                                         const int32_t* __restrict__ xp_rows,
+                                                         int64_t xp_bytes,
                                                          const bf16_t* __restrict__ w_gate,
                                                          const bf16_t* __restrict__ w_up,
                                                          const int32_t* __restrict__ offsets,
@@ -62,8 +68,11 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
     const int n0 = t.nt * C::BNS;
     const int64_t wofs = static_cast<int64_t>(t.e) * H * F + n0;
     const bf16_t* bs[2] = {w_gate + wofs, w_up + wofs};
-    gemm_mainloop<C, true, false>(xp + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, F, F - n0, H, smem,
-                                  acc);
+    if constexpr (kRows)
+      gemm_mainloop<C, true, false>(xp, H, t.m_lim, bs, F, F - n0, H, smem, acc, xp_rows + t.m0, xp_bytes);
+    else
+      gemm_mainloop<C, true, false>(xp + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, F, F - n0, H, smem,
+                                    acc);
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -77,9 +86,11 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
         f32x4 av;
 #pragma unroll
         for (int i = 0; i < 4; ++i) av[i] = silu_f(gv[i]) * uv[i];
-        *reinterpret_cast<uint2*>(g_out + base + c) = pack4_bf16(gv);
-        *reinterpret_cast<uint2*>(u_out + base + c) = pack4_bf16(uv);
-        *reinterpret_cast<uint2*>(a_out + base + c) = pack4_bf16(av);
+        if (g_out != nullptr) {
+          *reinterpret_cast<uint2*>(g_out + base + c) = pack4_bf16(gv);
+          *reinterpret_cast<uint2*>(u_out + base + c) = pack4_bf16(uv);
+        }
+        if (a_out != nullptr) *reinterpret_cast<uint2*>(a_out + base + c) = pack4_bf16(av);
       }
     }
   });
@@ -116,12 +127,15 @@ __global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restri
 
 // dA = dO W_down[e]^T (K = H, N = F) fused with the SwiGLU backward:
 // s = sigmoid(G); dG = dA U s (1 + G (1 - s)); dU = dA G s.
+// dG and dU may overwrite G and U in place: each lane reads an element of G
+// and U before it writes the same element of dG and dU, and nothing else
+// reads them.
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
-    const bf16_t* __restrict__ d_o, const bf16_t* __restrict__ w_down, const bf16_t* __restrict__ g_in,
-    const bf16_t* __restrict__ u_in, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, int E, int H, int F, bf16_t* __restrict__ dg_out,
-    bf16_t* __restrict__ du_out) {
+    const bf16_t* __restrict__ d_o, const bf16_t* __restrict__ w_down, const bf16_t* g_in,
+    const bf16_t* u_in, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ tile_start, int E, int H, int F, bf16_t* dg_out,
+    bf16_t* du_out) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
   for_each_grouped_tile(offsets, tile_start, E, F / C::BN, [&](const MTile& t) {
@@ -414,14 +428,15 @@ void gateup_wgrad_any(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, v
 
 }  // namespace
 
-hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s) {
+hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute) {
   using C = GateUpFwd;
-  const int grid = persistent_grid(k_gateup_fwd, C::kThreads,
-                                   static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
+  auto k = a.xp_rows != nullptr ? k_gateup_fwd<true> : k_gateup_fwd<false>;
+  const int grid =
+      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
   {
-    TraceScope trace_scope(K_GATEUP_FWD, s);
-    hipLaunchKernelGGL(k_gateup_fwd, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.w_gate, a.w_up, a.offsets,
-                       a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
+    TraceScope trace_scope(recompute ? K_GATEUP_RECOMPUTE : K_GATEUP_FWD, s);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.xp_rows, a.xp_bytes, a.w_gate, a.w_up,
+                       a.offsets, a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
   }
   return hipGetLastError();
 }

@@ -101,6 +101,20 @@ struct LoadKc {
       off[i] = static_cast<uint32_t>((q >> 3) * ld2 + ((q & 7) << 4));
     }
   }
+  // Rows through an index: tile row r is row rows[r] of src for r < r_lim;
+  // `bytes` (< 2^31) bounds the whole source.
+  __device__ __forceinline__ void init_rows(const bf16_t* src, int64_t ld, const int32_t* rows, int r_lim,
+                                            int64_t bytes, int tid) {
+    base = reinterpret_cast<const char*>(src);
+    ld2 = ld * 2;
+    valid = bytes;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int q = i * kThreads + tid;
+      const int r = q >> 3;
+      off[i] = r < r_lim ? static_cast<uint32_t>(rows[r] * ld2 + ((q & 7) << 4)) : kOob;
+    }
+  }
   __device__ __forceinline__ void disable() { valid = 0; }
   __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int K, int tid) const {
     const int64_t step = static_cast<int64_t>(kt) * (BK * 2);
@@ -261,12 +275,15 @@ __device__ __forceinline__ void interleave() {
 //   m_lim  valid rows of the tile (<= BM); K = number of valid k
 //   b[i]   tile origins of the NB B operands in layout B_KC, leading dim ldb
 //   n_lim  valid columns of each B operand (multiple of 8)
+//   a_rows if non-null (K-contiguous A only), tile row r is row a_rows[r] of
+//          the matrix at `a`, whose a_bytes (< 2^31) bound every access
 // Software pipeline: global loads run two K steps ahead of the MFMAs in two
 // register sets; LDS holds two stages; one LDS barrier per step.
 template <class C, bool A_KC, bool B_KC>
 __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int m_lim,
                                               const bf16_t* const* b, int64_t ldb, int n_lim, int K,
-                                              char* smem, f32x4 (&acc)[C::FM][C::FN]) {
+                                              char* smem, f32x4 (&acc)[C::FM][C::FN],
+                                              const int32_t* a_rows = nullptr, int64_t a_bytes = 0) {
   using LA = Loader<A_KC, C::BM, C::BM, C::kThreads>;
   using LB = Loader<B_KC, C::BNS, C::BN, C::kThreads>;
   const int tid = threadIdx.x;
@@ -276,7 +293,12 @@ __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int 
   if (nk <= 0) return;
   LA la;
   LB lb[C::NB];
-  la.setup(a, lda, m_lim, K, tid);
+  if constexpr (A_KC) {
+    if (a_rows != nullptr) la.init_rows(a, lda, a_rows, m_lim, a_bytes, tid);
+    else la.setup(a, lda, m_lim, K, tid);
+  } else {
+    la.setup(a, lda, m_lim, K, tid);
+  }
 #pragma unroll
   for (int i = 0; i < C::NB; ++i) lb[i].setup(b[i], ldb, n_lim, K, tid);
   uint4 ra[2][LA::kPer];

@@ -23,12 +23,18 @@ struct ExpertArgs {
   bf16_t* g;    // forward writes, backward reads
   bf16_t* u;
   bf16_t* act;  // A = silu(G) * U
+  // Gate/up forward only: when non-null, product row r reads row xp_rows[r]
+  // of xp (then the unpermuted tokens, xp_bytes < 2^31 bytes in all).
+  const int32_t* xp_rows = nullptr;
+  int64_t xp_bytes = 0;
 };
 
 int max_row_tiles(int rows_cap, int E);
 
-// G, U, A from Xp (gate/up products + SwiGLU).
-hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s);
+// G, U, A from Xp (gate/up products + SwiGLU); G and U are skipped when
+// a.g is null, A when a.act is.  `recompute` only names the launch in traces
+// (the backward's recomputation of G and U).
+hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute = false);
 // O = A W_down per expert.
 hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s);
 // dG, dU, dXp and the three weight gradients from dO.
@@ -46,7 +52,7 @@ hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* 
 // Workspace ints the permutation needs for T tokens and E experts.
 int64_t permute_ws_ints(int T, int E);
 // counts, offsets, tile_start, row_token (-1 beyond R), row_of from topk_idx;
-// then xp[r] = x[row_token[r]].
+// then xp[r] = x[row_token[r]] (skipped when xp is null).
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
                           int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);

@@ -61,7 +61,8 @@ int check_dims(const moe_dims* d) {
   if (d->E % 8 != 0) return fail(MOE_ERR_SHAPE, "E=%d must be a multiple of 8", d->E);
   if (static_cast<int64_t>(d->T) * d->top_k > (1ll << 30))
     return fail(MOE_ERR_ARG, "T*top_k=%lld too large", static_cast<long long>(d->T) * d->top_k);
-  if (d->flags & ~(MOE_F_MASK | MOE_F_DW_FP32)) return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
+  if (d->flags & ~(MOE_F_MASK | MOE_F_DW_FP32 | MOE_F_RECOMPUTE))
+    return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
   return MOE_OK;
 }
 
@@ -74,7 +75,7 @@ int check_experts_dims(const moe_experts_dims* d) {
   if (d->H % 128 != 0 || d->F % 128 != 0)
     return fail(MOE_ERR_SHAPE, "H=%d and F=%d must be multiples of 128", d->H, d->F);
   if (d->rows > (1 << 30)) return fail(MOE_ERR_ARG, "rows=%d too large", d->rows);
-  if (d->flags & ~MOE_F_DW_FP32) return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
+  if (d->flags & ~(MOE_F_DW_FP32 | MOE_F_RECOMPUTE)) return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
   return MOE_OK;
 }
 
@@ -108,8 +109,9 @@ Saved saved_layout(const moe_dims* d, void* base) {
   s.row_token = c.take<int32_t>(R);
   s.row_of = c.take<int32_t>(T * k);
   s.xp = c.take<bf16_t>(R * H);
-  s.g = c.take<bf16_t>(R * F);
-  s.u = c.take<bf16_t>(R * F);
+  const bool keep_gu = !(d->flags & MOE_F_RECOMPUTE);
+  s.g = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
+  s.u = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
   s.a = c.take<bf16_t>(R * F);
   s.o = c.take<bf16_t>(R * H);
   s.bytes = c.off;
@@ -142,6 +144,42 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
   return w;
 }
 
+// ---- layout of the forward-only (serving) workspace: routing, the permuted
+// rows only when x is too large to be read through the permutation, A and O.
+struct InferWs {
+  float* logits;
+  int32_t *topk_idx, *counts, *offsets, *tile_start, *row_token, *row_of, *perm;
+  float* gates;
+  bf16_t *xp, *a, *o;
+  size_t bytes;
+};
+
+// The gate/up product reads x through the permutation when a 32-bit buffer
+// offset reaches all of x.
+bool infer_reads_x(const moe_dims* d) {
+  return static_cast<int64_t>(d->T) * d->H * 2 <= 0x7fffffffll;
+}
+
+InferWs infer_layout(const moe_dims* d, void* base) {
+  const size_t T = d->T, E = d->E, k = d->top_k, H = d->H, F = d->F, R = T * k;
+  Carve c(base);
+  InferWs w;
+  w.logits = c.take<float>(T * E);
+  w.topk_idx = c.take<int32_t>(T * k);
+  w.gates = c.take<float>(T * k);
+  w.counts = c.take<int32_t>(E);
+  w.offsets = c.take<int32_t>(E + 1);
+  w.tile_start = c.take<int32_t>(E + 1);
+  w.row_token = c.take<int32_t>(R);
+  w.row_of = c.take<int32_t>(T * k);
+  w.perm = c.take<int32_t>(static_cast<size_t>(permute_ws_ints(d->T, d->E)));
+  w.xp = infer_reads_x(d) ? nullptr : c.take<bf16_t>(R * H);
+  w.a = c.take<bf16_t>(R * F);
+  w.o = c.take<bf16_t>(R * H);
+  w.bytes = c.off;
+  return w;
+}
+
 struct ExpSaved {
   int32_t *offsets, *tile_start;
   bf16_t *g, *u, *a;
@@ -154,8 +192,9 @@ ExpSaved exp_saved_layout(const moe_experts_dims* d, void* base) {
   ExpSaved s;
   s.offsets = c.take<int32_t>(E + 1);
   s.tile_start = c.take<int32_t>(E + 1);
-  s.g = c.take<bf16_t>(R * F);
-  s.u = c.take<bf16_t>(R * F);
+  const bool keep_gu = !(d->flags & MOE_F_RECOMPUTE);
+  s.g = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
+  s.u = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
   s.a = c.take<bf16_t>(R * F);
   s.bytes = c.off;
   return s;
@@ -179,6 +218,22 @@ ExpWs exp_ws_layout(const moe_experts_dims* d, void* base) {
 int hip_status(hipError_t e, const char* where) {
   if (e != hipSuccess) return fail(MOE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
   return ok();
+}
+
+// MOE_F_RECOMPUTE: the forward kept no G and U.  Recompute them with the
+// forward's kernel (same tiles, same summation order: the same bits) into the
+// dG / dU workspace, where the down dgrad then overwrites them in place.
+int recompute_gu(uint32_t flags, ExpertArgs& a, bf16_t* dg, bf16_t* du, hipStream_t s) {
+  if (!(flags & MOE_F_RECOMPUTE)) return MOE_OK;
+  ExpertArgs r = a;
+  r.g = dg;
+  r.u = du;
+  r.act = nullptr;
+  const hipError_t e = launch_gateup_fwd(r, s, /*recompute=*/true);
+  if (e != hipSuccess) return hip_status(e, "gate/up recompute");
+  a.g = dg;
+  a.u = du;
+  return MOE_OK;
 }
 
 }  // namespace
@@ -269,6 +324,7 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
+  if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // dXp reuses dO's memory: the down products that read dO are queued first.
   e = launch_experts_bwd(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_gate, dw_up, dw_down, f32, s);
   if (e != hipSuccess) return hip_status(e, "experts bwd");
@@ -277,6 +333,45 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
                        w.w_rt, static_cast<bf16_t*>(dx), s);
   return hip_status(e, "dx");
+}
+
+size_t moe_infer_workspace_bytes(const moe_dims* d) {
+  if (check_dims(d) != MOE_OK) return 0;
+  return infer_layout(d, nullptr).bytes;
+}
+
+int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+              const void* w_down, const uint8_t* token_mask, void* y, void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"y", y}, {"ws", ws}}))
+    return rc;
+  const bool masked = d->flags & MOE_F_MASK;
+  if (masked && token_mask == nullptr) return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
+  const InferWs w = infer_layout(d, ws);
+  if (ws_bytes < w.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
+  const bf16_t* xb = static_cast<const bf16_t*>(x);
+  hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
+                                   E, k, w.logits, w.topk_idx, w.gates, s);
+  if (e != hipSuccess) return hip_status(e, "router");
+  e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.row_token, w.row_of,
+                     w.xp, w.perm, s);
+  if (e != hipSuccess) return hip_status(e, "permute");
+  ExpertArgs a{T * k, H, E, F, w.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+               static_cast<const bf16_t*>(w_down), w.offsets, w.tile_start, nullptr, nullptr, w.a};
+  if (w.xp == nullptr) {
+    a.xp = xb;
+    a.xp_rows = w.row_token;
+    a.xp_bytes = static_cast<int64_t>(T) * H * 2;
+  }
+  e = launch_gateup_fwd(a, s);
+  if (e != hipSuccess) return hip_status(e, "gate/up");
+  e = launch_down_fwd(a, w.o, s);
+  if (e != hipSuccess) return hip_status(e, "down");
+  e = launch_combine(w.o, w.gates, w.row_of, T, H, k, static_cast<bf16_t*>(y), s);
+  return hip_status(e, "combine");
 }
 
 size_t moe_experts_saved_bytes(const moe_experts_dims* d) {
@@ -337,6 +432,7 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
   ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
                static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
                sv.g, sv.u, sv.a};
+  if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   hipError_t e = launch_experts_bwd(a, static_cast<const bf16_t*>(d_o), w.dg, w.du, static_cast<bf16_t*>(dxp),
                                     dw_gate, dw_up, dw_down, (d->flags & MOE_F_DW_FP32) != 0, s);
   return hip_status(e, "experts bwd");
@@ -344,6 +440,6 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
 
 const char* moe_last_error(void) { return g_err; }
 
-int moe_version(void) { return 100; }
+int moe_version(void) { return 101; }
 
 }  // extern "C"

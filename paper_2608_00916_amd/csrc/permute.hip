@@ -196,6 +196,7 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
     hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
                        row_token, row_of);
   }
+  if (xp == nullptr) return hipGetLastError();
   const int grid = static_cast<int>(std::min<int64_t>(cdiv64(static_cast<int64_t>(T) * k, 4), 8192));
   {
     TraceScope trace_scope(K_GATHER, s);

@@ -28,6 +28,7 @@ enum KernelId {
   K_ROUTER_DX,
   K_OFFSETS,
   K_TRANSPOSE_WR,
+  K_GATEUP_RECOMPUTE,
   K_NUM_KERNELS
 };
 

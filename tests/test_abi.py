@@ -137,3 +137,21 @@ def test_trace_api_without_launches():
     names = {L.moe_trace_name(i).decode() for i in range(n)}
     assert {"gateup_fwd", "gateup_wgrad", "combine", "topk"} <= names
     assert L.moe_trace_name(-1).decode() == ""
+
+
+def test_recompute_flag_layout():
+    """MOE_F_RECOMPUTE drops G and U from the saved buffer (views NULL)."""
+    L = _lib.lib()
+    d, dr = D(), D(flags=_lib.MOE_F_RECOMPUTE)
+    R, F = 256 * 2, 256
+    assert L.moe_saved_bytes(ctypes.byref(d)) - L.moe_saved_bytes(ctypes.byref(dr)) == 2 * R * F * 2
+    v = _lib.MoeSavedView()
+    assert L.moe_saved_views(ctypes.byref(dr), 1 << 20, ctypes.byref(v)) == 0
+    assert v.g is None and v.u is None and v.a is not None and v.o is not None
+    ed = _lib.MoeExpertsDims(1000, 256, 4, 128, _lib.MOE_F_RECOMPUTE)
+    ev = _lib.MoeExpertsSavedView()
+    assert L.moe_experts_saved_views(ctypes.byref(ed), 1 << 20, ctypes.byref(ev)) == 0
+    assert ev.g is None and ev.u is None and ev.a is not None
+    full = _lib.MoeExpertsDims(1000, 256, 4, 128, 0)
+    assert (L.moe_experts_saved_bytes(ctypes.byref(full)) - L.moe_experts_saved_bytes(ctypes.byref(ed))
+            == 2 * 1000 * 128 * 2)

@@ -24,15 +24,15 @@ def oracle_run(inp):
     return f, b
 
 
-def gpu_run(inp, dw_fp32=False, repeat=1):
+def gpu_run(inp, dw_fp32=False, repeat=1, recompute=False):
     import torch
     import paper_2608_00916_amd as moe
     d = inp["dims"]
     mask = inp["mask"]
     print(f"GPU block T={d['T']} H={d['H']} E={d['E']} k={d['k']} F={d['F']} "
-          f"mask={mask is not None} dw_fp32={dw_fp32}", flush=True)
+          f"mask={mask is not None} dw_fp32={dw_fp32} recompute={recompute}", flush=True)
     blk = moe.MoEBlock(d["T"], d["H"], d["E"], d["F"], d["k"], mask=mask is not None,
-                       dw_fp32=dw_fp32)
+                       dw_fp32=dw_fp32, recompute=recompute)
     t = {n: dev_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
     tm = None if mask is None else torch.from_numpy(mask.astype(np.uint8)).cuda()
     outs = []
@@ -45,7 +45,7 @@ def gpu_run(inp, dw_fp32=False, repeat=1):
         out = {n: host(v[n]) for n in ("logits", "topk_idx", "gates", "counts", "offsets",
                                       "row_token", "row_of")}
         for n in ("xp", "g", "u", "a", "o"):
-            out[n] = host(v[n][:R])
+            out[n] = None if v[n] is None else host(v[n][:R])
         out.update(y=host(blk.y), dx=host(blk.dx), dw_r=host(blk.dw_r), dw_gate=host(blk.dw_gate),
                    dw_up=host(blk.dw_up), dw_down=host(blk.dw_down))
         outs.append(out)
@@ -148,3 +148,20 @@ def test_bitwise_deterministic():
     a, c = gpu_run(inp, repeat=2)
     for n in a:
         assert np.array_equal(a[n], c[n]), n
+
+
+def test_recompute_is_bit_identical():
+    """MOE_F_RECOMPUTE: the forward keeps no G and U and the backward
+    recomputes them with the same kernel, so every output and gradient is
+    bit-identical to the run that kept them (which is checked against the
+    oracle here too)."""
+    inp = workloads.block_inputs(T=777, H=256, E=16, k=4, F=384, seed=43)
+    inp["mask"] = (np.arange(777) % 5 != 3).astype(np.uint8)
+    f, b = oracle_run(inp)
+    a = gpu_run(inp)
+    compare(inp, a, f, b)
+    r = gpu_run(inp, recompute=True)
+    assert r["g"] is None and r["u"] is None
+    for n in a:
+        if n not in ("g", "u"):
+            assert np.array_equal(a[n], r[n]), n

@@ -69,3 +69,32 @@ def test_counts_overflow_capacity():
 
 def test_fp32_weight_grads():
     run(512, 256, 3, 128, [200, 150, 162], seed=4, dw_fp32=True)
+
+
+def test_recompute_is_bit_identical():
+    """The experts path with MOE_F_RECOMPUTE matches the run that kept G and U
+    bit for bit."""
+    import torch
+    import paper_2608_00916_amd as moe
+    rows, H, E, F = 700, 256, 6, 256
+    counts = np.array([130, 0, 257, 1, 0, 300], dtype=np.int32)
+    s = np.random.SeedSequence(5).spawn(5)
+    t = {n: dev_bf16(workloads.normal_bf16(q, shape, std)) for n, q, shape, std in (
+        ("xp", s[0], (rows, H), 1.0), ("wg", s[1], (E, H, F), 0.02), ("wu", s[2], (E, H, F), 0.02),
+        ("wd", s[3], (E, F, H), 0.02), ("d_o", s[4], (rows, H), 1.0))}
+    print(f"GPU experts recompute rows={rows} H={H} E={E} F={F}", flush=True)
+    c = torch.from_numpy(counts).cuda()
+    outs = []
+    for recompute in (False, True):
+        ex = moe.MoEExperts(rows, H, E, F, recompute=recompute)
+        ex.o.zero_()
+        ex.dxp.zero_()
+        ex.forward(t["xp"], c, t["wg"], t["wu"], t["wd"])
+        ex.backward(t["xp"], t["wg"], t["wu"], t["wd"], t["d_o"])
+        torch.cuda.synchronize()
+        outs.append({n: host(getattr(ex, n)) for n in ("o", "dxp", "dw_gate", "dw_up", "dw_down")})
+        outs[-1]["a"] = host(ex.views["a"][:int(counts.sum())])  # rows past the counts are undefined
+        if recompute:
+            assert ex.views["g"] is None and ex.views["u"] is None
+    for n in outs[0]:
+        assert np.array_equal(outs[0][n], outs[1][n]), n

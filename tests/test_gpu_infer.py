@@ -1,0 +1,102 @@
+"""GPU parity of the forward-only (serving) entry point moe_infer.
+
+It runs the training forward's kernels except that the gate/up product reads
+its rows of x through the permutation and G, U are never stored, so its Y must
+equal moe_fwd's bit for bit; it is also compared with the oracle."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import moe_oracle as O
+from tests.parity import assert_close, check_routing, dev_bf16, host
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "tiny": None,
+    "ragged_multi_tile": dict(T=1000, H=512, E=8, k=2, F=384, seed=21),
+    "single_token": dict(T=1, H=128, E=8, k=2, F=128, seed=23),
+    "max_E_max_k": dict(T=100, H=128, E=256, k=32, F=128, seed=26),
+    "empty_experts": dict(T=257, H=256, E=32, k=3, F=128, seed=27, zipf_s=1.2, n_cold=6),
+    "masked": dict(T=333, H=256, E=16, k=2, F=128, seed=31),
+}
+
+
+def run_both(inp):
+    import torch
+    import paper_2608_00916_amd as moe
+    d = inp["dims"]
+    mask = inp["mask"]
+    print(f"GPU infer T={d['T']} H={d['H']} E={d['E']} k={d['k']} F={d['F']} mask={mask is not None}",
+          flush=True)
+    t = {n: dev_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down")}
+    tm = None if mask is None else torch.from_numpy(mask.astype(np.uint8)).cuda()
+    blk = moe.MoEBlock(d["T"], d["H"], d["E"], d["F"], d["k"], mask=tm is not None)
+    blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+    inf = moe.MoEInfer(d["T"], d["H"], d["E"], d["F"], d["k"], mask=tm is not None)
+    inf.y.fill_(7.0)
+    inf.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+    torch.cuda.synchronize()
+    v = blk.views
+    return host(inf.y), host(blk.y), {n: host(v[n]) for n in ("logits", "topk_idx", "gates")}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_infer_matches_forward_and_oracle(case):
+    if CASES[case] is None:
+        inp = workloads.make(case)
+    else:
+        inp = workloads.block_inputs(**CASES[case])
+    if case == "masked":
+        inp["mask"] = (np.random.default_rng(5).random(inp["dims"]["T"]) > 0.3).astype(np.uint8)
+    y_inf, y_fwd, routing = run_both(inp)
+    assert np.array_equal(y_inf, y_fwd), "moe_infer and moe_fwd differ"
+    d = inp["dims"]
+    w = {n: O.widen_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down")}
+    mask = None if inp["mask"] is None else inp["mask"].astype(bool)
+    f = O.moe_forward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], d["k"], mask)
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], routing["logits"], routing["topk_idx"],
+                                  routing["gates"], d["k"], mask)
+    keep = ~flipped
+    assert_close("y", y_inf[keep], f["Y"][keep])
+
+
+def test_infer_qwen3_30b_a3b_fullsize():
+    """T=8192, H=2048, E=128, top-8, F=768: bitwise equal to the training forward."""
+    inp = workloads.make("qwen3_30b_a3b")
+    y_inf, y_fwd, _ = run_both(inp)
+    assert np.array_equal(y_inf, y_fwd)
+
+
+def test_infer_copies_rows_when_x_exceeds_buffer_range():
+    """x of 2 GiB (T = 2^20, H = 1024): past the reach of 32-bit buffer
+    offsets, so moe_infer gathers the rows into its workspace instead; still
+    bitwise equal to moe_fwd, and equal to the oracle on sampled tokens."""
+    import torch
+    import paper_2608_00916_amd as moe
+    T, H, E, k, F = 1 << 20, 1024, 8, 1, 128
+    print(f"GPU infer large x T={T} H={H} E={E} k={k} F={F}", flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    x = torch.randn((T, H), generator=g, device="cuda").to(torch.bfloat16)
+    w_r = (0.02 * torch.randn((H, E), generator=g, device="cuda")).to(torch.bfloat16)
+    w_gate = (0.02 * torch.randn((E, H, F), generator=g, device="cuda")).to(torch.bfloat16)
+    w_up = (0.02 * torch.randn((E, H, F), generator=g, device="cuda")).to(torch.bfloat16)
+    w_down = (0.02 * torch.randn((E, F, H), generator=g, device="cuda")).to(torch.bfloat16)
+    inf = moe.MoEInfer(T, H, E, F, k)
+    assert moe.moe_infer_workspace_bytes(inf.d) >= T * k * H * 2 * 2  # the row copy and O
+    inf.forward(x, w_r, w_gate, w_up, w_down)
+    blk = moe.MoEBlock(T, H, E, F, k)
+    blk.forward(x, w_r, w_gate, w_up, w_down)
+    torch.cuda.synchronize()
+    assert torch.equal(inf.y, blk.y)
+    S = np.sort(np.random.default_rng(3).choice(T, 64, replace=False))
+    Si = torch.from_numpy(S).cuda()
+
+    def h(t):
+        return O.widen_bf16(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+    f = O.moe_forward(h(x[Si]), h(w_r), h(w_gate), h(w_up), h(w_down), k, None)
+    y = h(inf.y[Si])
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], host(blk.views["logits"][Si]),
+                                  host(blk.views["topk_idx"][Si]), host(blk.views["gates"][Si]), k, None)
+    assert_close("y[S]", y[~flipped], f["Y"][~flipped])
