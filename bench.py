@@ -51,10 +51,10 @@ def kernel_work(name, T, Tv, H, E, F, k, R):
         "gateup_dgrad": ("flop", 4.0 * H * F * R),
         "gateup_wgrad": ("flop", 4.0 * H * F * R),
         "dwr_partial": ("flop", 2.0 * Tv * H * E),
-        "router_dx": ("flop", 2.0 * Tv * H * E),
-        "gather": ("byte", float(Tv * H * b + R * H * b)),
+        "permute_rows": ("byte", float(Tv * H * b + R * H * b)),
         "combine": ("byte", float(R * H * b + Tv * H * b)),
         "combine_bwd": ("byte", float(Tv * H * b + 2 * R * H * b)),
+        "router_dx": ("byte", float(R * H * b + Tv * H * b)),
     }.get(name, ("none", 0.0))
 
 

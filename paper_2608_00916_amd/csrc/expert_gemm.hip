@@ -447,9 +447,8 @@ hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
-                              bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
-                              hipStream_t s) {
+hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
+                                   bf16_t* dxp, void* dw_down, bool dw_f32, hipStream_t s) {
   const bool f256 = a.F % 256 == 0, h256 = a.H % 256 == 0;
   if (f256) down_dgrad<Wide>(a, d_o, dg, du, s);
   else down_dgrad<Narrow>(a, d_o, dg, du, s);
@@ -457,8 +456,21 @@ hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg
   else down_wgrad_any<Narrow>(a, d_o, dw_down, dw_f32, s);
   if (h256) gateup_dgrad<Wide>(a, dg, du, dxp, s);
   else gateup_dgrad<Narrow>(a, dg, du, dxp, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate,
+                                       void* dw_up, bool dw_f32, hipStream_t s) {
   gateup_wgrad_any<WideGU>(a, dg, du, dw_gate, dw_up, dw_f32, s);
   return hipGetLastError();
+}
+
+hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
+                              bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
+                              hipStream_t s) {
+  const hipError_t e = launch_experts_bwd_data(a, d_o, dg, du, dxp, dw_down, dw_f32, s);
+  if (e != hipSuccess) return e;
+  return launch_experts_bwd_gateup_w(a, dg, du, dw_gate, dw_up, dw_f32, s);
 }
 
 }  // namespace moe

@@ -41,6 +41,13 @@ hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s);
 hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
                               bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
                               hipStream_t s);
+// The same in two parts, so that work can be queued between them: dG, dU,
+// dW_down and dXp (dxp may alias d_o: it is written last) ...
+hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
+                                   bf16_t* dxp, void* dw_down, bool dw_f32, hipStream_t s);
+// ... then dW_gate and dW_up.
+hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate,
+                                       void* dw_up, bool dw_f32, hipStream_t s);
 
 // ---- routing (router.hip)
 // logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
@@ -52,7 +59,8 @@ hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* 
 // Workspace ints the permutation needs for T tokens and E experts.
 int64_t permute_ws_ints(int T, int E);
 // counts, offsets, tile_start, row_token (-1 beyond R), row_of from topk_idx;
-// then xp[r] = x[row_token[r]] (skipped when xp is null).
+// then xp[r] = x[row_token[r]], written token-major through row_of (skipped
+// when xp is null).
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
                           int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);

@@ -326,13 +326,16 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // dXp reuses dO's memory: the down products that read dO are queued first.
-  e = launch_experts_bwd(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_gate, dw_up, dw_down, f32, s);
+  e = launch_experts_bwd_data(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_down, f32, s);
   if (e != hipSuccess) return hip_status(e, "experts bwd");
-  e = launch_dwr(static_cast<const bf16_t*>(x), w.dz, T, H, E, w.dwr_part, dw_r, f32, s);
-  if (e != hipSuccess) return hip_status(e, "router weight grad");
+  // dX right after dXp, while much of dXp is still in the last-level cache.
   e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
                        w.w_rt, static_cast<bf16_t*>(dx), s);
-  return hip_status(e, "dx");
+  if (e != hipSuccess) return hip_status(e, "dx");
+  e = launch_experts_bwd_gateup_w(a, w.dg, w.du, dw_gate, dw_up, f32, s);
+  if (e != hipSuccess) return hip_status(e, "experts bwd");
+  e = launch_dwr(static_cast<const bf16_t*>(x), w.dz, T, H, E, w.dwr_part, dw_r, f32, s);
+  return hip_status(e, "router weight grad");
 }
 
 size_t moe_infer_workspace_bytes(const moe_dims* d) {

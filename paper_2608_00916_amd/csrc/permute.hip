@@ -125,27 +125,43 @@ __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restri
   }
 }
 
-// xp[r] = x[row_token[r]] for r < offsets[E]: one wave per row, 16 bytes per
-// lane per pass, four passes' loads issued before their stores.
-__global__ __launch_bounds__(256) void k_gather(const bf16_t* __restrict__ x,
-                                                const int32_t* __restrict__ row_token,
-                                                const int32_t* __restrict__ offsets, int E, int H,
-                                                bf16_t* __restrict__ xp) {
-  const int64_t R = offsets[E];
+// xp[row_of[t,j]] = x[t] for every routed slot (the same rows as
+// xp[r] = x[row_token[r]]), token-major: one wave per token reads its row of
+// x once, 16 bytes per lane, and writes it to the token's k permuted rows.
+// The stores are non-temporal: Xp is next read by the gate/up product, long
+// after it would have left the caches.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int KT>
+__global__ __launch_bounds__(256) void k_permute_rows(const bf16_t* __restrict__ x,
+                                                      const int32_t* __restrict__ row_of, int T, int H, int k,
+                                                      bf16_t* __restrict__ xp) {
   const int lane = threadIdx.x & 63;
   const int64_t nwaves = static_cast<int64_t>(gridDim.x) * 4;
-  for (int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); r < R; r += nwaves) {
-    const bf16_t* src = x + static_cast<int64_t>(row_token[r]) * H;
-    bf16_t* dst = xp + r * H;
-    int c = lane * 8;
-    for (; c + 3 * 512 < H; c += 4 * 512) {
-      uint4 v[4];
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6); t < T; t += nwaves) {
+    int rows[KT];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = *reinterpret_cast<const uint4*>(src + c + i * 512);
+    for (int j = 0; j < KT; ++j) rows[j] = j < k ? row_of[t * k + j] : -1;
+    if (rows[0] < 0) continue;  // a masked token has no rows
+    const bf16_t* src = x + t * H;
+    for (int c0 = lane * 8; c0 < H; c0 += 4 * kWave * 8) {
+      u32x4_t v[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(dst + c + i * 512) = v[i];
+      for (int i = 0; i < 4; ++i) {
+        const int c = c0 + i * kWave * 8;
+        v[i] = c < H ? *reinterpret_cast<const u32x4_t*>(src + c) : u32x4_t{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int j = 0; j < KT; ++j) {
+        if (rows[j] < 0) continue;
+        bf16_t* dst = xp + static_cast<int64_t>(rows[j]) * H;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int c = c0 + i * kWave * 8;
+          if (c < H) __builtin_nontemporal_store(v[i], reinterpret_cast<u32x4_t*>(dst + c));
+        }
+      }
     }
-    for (; c < H; c += 512) *reinterpret_cast<uint4*>(dst + c) = *reinterpret_cast<const uint4*>(src + c);
   }
 }
 
@@ -197,10 +213,16 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
                        row_token, row_of);
   }
   if (xp == nullptr) return hipGetLastError();
-  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(static_cast<int64_t>(T) * k, 4), 8192));
+  // a few waves per CU suffice: each token's row is read once and written k times
+  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(T, 4), 1024));
   {
-    TraceScope trace_scope(K_GATHER, s);
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, x, row_token, offsets, E, H, xp);
+    TraceScope trace_scope(K_PERMUTE_ROWS, s);
+    if (k <= 1) hipLaunchKernelGGL(k_permute_rows<1>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
+    else if (k <= 2) hipLaunchKernelGGL(k_permute_rows<2>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
+    else if (k <= 4) hipLaunchKernelGGL(k_permute_rows<4>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
+    else if (k <= 8) hipLaunchKernelGGL(k_permute_rows<8>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
+    else if (k <= 16) hipLaunchKernelGGL(k_permute_rows<16>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
+    else hipLaunchKernelGGL(k_permute_rows<32>, dim3(grid), dim3(256), 0, s, x, row_of, T, H, k, xp);
   }
   return hipGetLastError();
 }

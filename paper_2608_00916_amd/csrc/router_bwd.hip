@@ -59,20 +59,19 @@ __global__ __launch_bounds__(256) void k_dwr_reduce(const float* __restrict__ pa
   }
 }
 
-// W_rT[E][H] = W_r[H][E] through 64 x 64 LDS tiles.
+// W_rT[E][H] = W_r[H][E] through 32 x 32 LDS tiles (grid H/32 x E/32).
 __global__ __launch_bounds__(256) void k_transpose_wr(const bf16_t* __restrict__ w_r, int H, int E,
                                                       bf16_t* __restrict__ w_rt) {
-  __shared__ bf16_t tile[64][65];
-  const int h0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int hh = i / 64, ee = i % 64;
-    if (h0 + hh < H && e0 + ee < E) tile[hh][ee] = w_r[static_cast<int64_t>(h0 + hh) * E + e0 + ee];
-  }
+  __shared__ bf16_t tile[32][33];
+  const int h0 = blockIdx.x * 32, e0 = blockIdx.y * 32;
+  const int a = threadIdx.x >> 5, b = threadIdx.x & 31;
+#pragma unroll
+  for (int i = 0; i < 32; i += 8)
+    if (h0 + a + i < H && e0 + b < E) tile[a + i][b] = w_r[static_cast<int64_t>(h0 + a + i) * E + e0 + b];
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-    const int ee = i / 64, hh = i % 64;
-    if (h0 + hh < H && e0 + ee < E) w_rt[static_cast<int64_t>(e0 + ee) * H + h0 + hh] = tile[hh][ee];
-  }
+#pragma unroll
+  for (int i = 0; i < 32; i += 8)
+    if (e0 + a + i < E && h0 + b < H) w_rt[static_cast<int64_t>(e0 + a + i) * H + h0 + b] = tile[b][a + i];
 }
 
 // dX[t] = sum_j ( dXp[row_of[t,j]] + dz_j W_r[:, idx_j] ): dz is non-zero on
@@ -151,7 +150,7 @@ hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const
                             bf16_t* w_rt, bf16_t* dx, hipStream_t s) {
   {
     TraceScope trace_scope(K_TRANSPOSE_WR, s);
-    hipLaunchKernelGGL(k_transpose_wr, dim3(cdiv(H, 64), cdiv(E, 64)), dim3(256), 0, s, w_r, H, E, w_rt);
+    hipLaunchKernelGGL(k_transpose_wr, dim3(cdiv(H, 32), cdiv(E, 32)), dim3(256), 0, s, w_r, H, E, w_rt);
   }
   {
     TraceScope trace_scope(K_ROUTER_DX, s);

@@ -14,7 +14,7 @@ enum KernelId {
   K_PERM_HIST,
   K_PERM_SCAN,
   K_PERM_SCATTER,
-  K_GATHER,
+  K_PERMUTE_ROWS,
   K_GATEUP_FWD,
   K_DOWN_FWD,
   K_COMBINE,
