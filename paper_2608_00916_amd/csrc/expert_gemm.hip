@@ -2,7 +2,7 @@
 //
 // Rows are grouped expert-major: expert e owns rows [offsets[e], offsets[e+1]).
 // Products over the rows of one expert (gate/up, down, and their input
-// gradients) walk a device-built table tile_start[E+1] of 128-row tiles, so the
+// gradients) walk a device-built table of 128-row tiles, so the
 // host never learns the counts: they run as persistent grids (a few workgroups
 // per CU) that stride over the tiles the table holds.  Weight gradients
 // (K = rows of one expert) have a fixed grid of E x (M/128) x (N/128) tiles;
@@ -27,18 +27,29 @@ struct MTile {
 // Run body(tile) for every (expert, row tile, column tile) of a grouped
 // product with n_ntiles column tiles.  Tile i*gridDim + xcd_tile(block) goes
 // to this workgroup in round i, so each XCD works on a contiguous run of tiles.
+// A tile's row range comes from one load of the tile table, issued a tile
+// ahead (always from a valid entry: a select between that load and a
+// register would turn it into a flat access, whose pending state makes every
+// LDS wait of the K loop a full drain).
 template <typename Body>
-__device__ __forceinline__ void for_each_grouped_tile(const int32_t* offsets, const int32_t* tile_start,
-                                                      int E, int n_ntiles, Body&& body) {
+__device__ __forceinline__ void for_each_grouped_tile(const int32_t* tile_start, const int2* tile_desc, int E,
+                                                      int n_ntiles, Body&& body) {
   const int total = tile_start[E] * n_ntiles;
-  for (int logical = xcd_tile(blockIdx.x, gridDim.x); logical < total; logical += gridDim.x) {
-    const int mt = logical / n_ntiles, nt = logical - mt * n_ntiles;
+  int logical = xcd_tile(blockIdx.x, gridDim.x);
+  if (logical >= total) return;
+  int2 d = tile_desc[logical / n_ntiles];
+  while (logical < total) {
+    const int mt = logical / n_ntiles;
+    const int next = logical + gridDim.x;
+    const int2 dn = tile_desc[min(next, total - 1) / n_ntiles];
     MTile t;
-    t.e = find_group(tile_start, E, mt);
-    t.m0 = offsets[t.e] + (mt - tile_start[t.e]) * kRowTile;
-    t.m_lim = min(kRowTile, offsets[t.e + 1] - t.m0);
-    t.nt = nt;
+    t.e = d.y & 0xff;
+    t.m_lim = d.y >> 8;
+    t.m0 = d.x;
+    t.nt = logical - mt * n_ntiles;
     body(t);
+    d = dn;
+    logical = next;
   }
 }
 
@@ -55,14 +66,14 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
                                                          const bf16_t* __restrict__ w_gate,
                                                          const bf16_t* __restrict__ w_up,
                                                          const int32_t* __restrict__ offsets,
-                                                         const int32_t* __restrict__ tile_start, int E,
+                                                         const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
                                                          int H, int F, bf16_t* __restrict__ g_out,
                                                          bf16_t* __restrict__ u_out,
                                                          bf16_t* __restrict__ a_out) {
   using C = GateUpFwd;
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(offsets, tile_start, E, F / C::BNS, [&](const MTile& t) {
+  for_each_grouped_tile(tile_start, tile_desc, E, F / C::BNS, [&](const MTile& t) {
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
     const int n0 = t.nt * C::BNS;
@@ -101,11 +112,11 @@ template <class C>
 __global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restrict__ act,
                                                        const bf16_t* __restrict__ w_down,
                                                        const int32_t* __restrict__ offsets,
-                                                       const int32_t* __restrict__ tile_start, int E,
+                                                       const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
                                                        int H, int F, bf16_t* __restrict__ o_out) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(offsets, tile_start, E, H / C::BN, [&](const MTile& t) {
+  for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
     const int n0 = t.nt * C::BN;
@@ -134,11 +145,11 @@ template <class C>
 __global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
     const bf16_t* __restrict__ d_o, const bf16_t* __restrict__ w_down, const bf16_t* g_in,
     const bf16_t* u_in, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, int E, int H, int F, bf16_t* dg_out,
+    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* dg_out,
     bf16_t* du_out) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(offsets, tile_start, E, F / C::BN, [&](const MTile& t) {
+  for_each_grouped_tile(tile_start, tile_desc, E, F / C::BN, [&](const MTile& t) {
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
     const int n0 = t.nt * C::BN;
@@ -179,10 +190,10 @@ template <class C>
 __global__ __launch_bounds__(C::kThreads) void k_gateup_dgrad(
     const bf16_t* __restrict__ dg_in, const bf16_t* __restrict__ du_in, const bf16_t* __restrict__ w_gate,
     const bf16_t* __restrict__ w_up, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, int E, int H, int F, bf16_t* __restrict__ dxp_out) {
+    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* __restrict__ dxp_out) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(offsets, tile_start, E, H / C::BN, [&](const MTile& t) {
+  for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
     const int n0 = t.nt * C::BN;
@@ -376,7 +387,7 @@ void down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   const int grid =
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_DOWN_FWD, s);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.act, a.w_down, a.offsets, a.tile_start, a.E,
+  hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.act, a.w_down, a.offsets, a.tile_start, a.tile_desc, a.E,
                      a.H, a.F, o);
 }
 
@@ -387,7 +398,7 @@ void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, 
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN));
   TraceScope trace_scope(K_DOWN_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start,
-                     a.E, a.H, a.F, dg, du);
+                     a.tile_desc, a.E, a.H, a.F, dg, du);
 }
 
 template <class C>
@@ -397,7 +408,7 @@ void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_GATEUP_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start,
-                     a.E, a.H, a.F, dxp);
+                     a.tile_desc, a.E, a.H, a.F, dxp);
 }
 
 template <class C, bool F32>
@@ -436,7 +447,7 @@ hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute)
   {
     TraceScope trace_scope(recompute ? K_GATEUP_RECOMPUTE : K_GATEUP_FWD, s);
     hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.xp_rows, a.xp_bytes, a.w_gate, a.w_up,
-                       a.offsets, a.tile_start, a.E, a.H, a.F, a.g, a.u, a.act);
+                       a.offsets, a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g, a.u, a.act);
   }
   return hipGetLastError();
 }

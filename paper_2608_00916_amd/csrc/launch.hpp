@@ -11,7 +11,8 @@ namespace moe {
 
 // Operands of the grouped expert products.  Rows are grouped expert-major;
 // offsets[E+1] and tile_start[E+1] (prefix sums of rows and of 128-row tiles
-// per expert) are device arrays.
+// per expert) and tile_desc[tile_start[E]] (per 128-row tile: first row,
+// expert | rows << 8) are device arrays.
 struct ExpertArgs {
   int rows_cap, H, E, F;
   const bf16_t* xp;
@@ -20,6 +21,7 @@ struct ExpertArgs {
   const bf16_t* w_down;
   const int32_t* offsets;
   const int32_t* tile_start;
+  const int2* tile_desc;
   bf16_t* g;    // forward writes, backward reads
   bf16_t* u;
   bf16_t* act;  // A = silu(G) * U
@@ -62,11 +64,12 @@ int64_t permute_ws_ints(int T, int E);
 // then xp[r] = x[row_token[r]], written token-major through row_of (skipped
 // when xp is null).
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
-                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
-                          int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);
-// offsets (clamped to rows) and tile_start from device counts (experts path).
+                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
+                          int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);
+// offsets (clamped to rows), tile_start and tile_desc from device counts
+// (experts path).
 hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, int32_t* offsets,
-                                      int32_t* tile_start, hipStream_t s);
+                                      int32_t* tile_start, int2* tile_desc, hipStream_t s);
 
 // ---- combine (combine.hip)
 // y[t] = sum_j gates[t,j] o[row_of[t,j]] (0 for masked tokens).

@@ -91,6 +91,7 @@ int check_ptrs(std::initializer_list<std::pair<const char*, const void*>> ps) {
 struct Saved {
   float* logits;
   int32_t *topk_idx, *counts, *offsets, *tile_start, *row_token, *row_of;
+  int2* tile_desc;
   float* gates;
   bf16_t *xp, *g, *u, *a, *o;
   size_t bytes;
@@ -106,6 +107,7 @@ Saved saved_layout(const moe_dims* d, void* base) {
   s.counts = c.take<int32_t>(E);
   s.offsets = c.take<int32_t>(E + 1);
   s.tile_start = c.take<int32_t>(E + 1);
+  s.tile_desc = c.take<int2>(static_cast<size_t>(max_row_tiles(d->T * d->top_k, d->E)));
   s.row_token = c.take<int32_t>(R);
   s.row_of = c.take<int32_t>(T * k);
   s.xp = c.take<bf16_t>(R * H);
@@ -149,6 +151,7 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
 struct InferWs {
   float* logits;
   int32_t *topk_idx, *counts, *offsets, *tile_start, *row_token, *row_of, *perm;
+  int2* tile_desc;
   float* gates;
   bf16_t *xp, *a, *o;
   size_t bytes;
@@ -170,6 +173,7 @@ InferWs infer_layout(const moe_dims* d, void* base) {
   w.counts = c.take<int32_t>(E);
   w.offsets = c.take<int32_t>(E + 1);
   w.tile_start = c.take<int32_t>(E + 1);
+  w.tile_desc = c.take<int2>(static_cast<size_t>(max_row_tiles(d->T * d->top_k, d->E)));
   w.row_token = c.take<int32_t>(R);
   w.row_of = c.take<int32_t>(T * k);
   w.perm = c.take<int32_t>(static_cast<size_t>(permute_ws_ints(d->T, d->E)));
@@ -182,6 +186,7 @@ InferWs infer_layout(const moe_dims* d, void* base) {
 
 struct ExpSaved {
   int32_t *offsets, *tile_start;
+  int2* tile_desc;
   bf16_t *g, *u, *a;
   size_t bytes;
 };
@@ -192,6 +197,7 @@ ExpSaved exp_saved_layout(const moe_experts_dims* d, void* base) {
   ExpSaved s;
   s.offsets = c.take<int32_t>(E + 1);
   s.tile_start = c.take<int32_t>(E + 1);
+  s.tile_desc = c.take<int2>(static_cast<size_t>(max_row_tiles(d->rows, d->E)));
   const bool keep_gu = !(d->flags & MOE_F_RECOMPUTE);
   s.g = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
   s.u = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
@@ -292,11 +298,11 @@ int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
                                    E, k, sv.logits, sv.topk_idx, sv.gates, s);
   if (e != hipSuccess) return hip_status(e, "router");
-  e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.row_token,
+  e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
                      sv.row_of, sv.xp, static_cast<int32_t*>(ws), s);
   if (e != hipSuccess) return hip_status(e, "permute");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
-               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
   e = launch_gateup_fwd(a, s);
   if (e != hipSuccess) return hip_status(e, "gate/up");
   e = launch_down_fwd(a, sv.o, s);
@@ -323,7 +329,7 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
                                     T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, s);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
-               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.g, sv.u, sv.a};
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // dXp reuses dO's memory: the down products that read dO are queued first.
   e = launch_experts_bwd_data(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_down, f32, s);
@@ -359,11 +365,11 @@ int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
                                    E, k, w.logits, w.topk_idx, w.gates, s);
   if (e != hipSuccess) return hip_status(e, "router");
-  e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.row_token, w.row_of,
+  e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.tile_desc, w.row_token, w.row_of,
                      w.xp, w.perm, s);
   if (e != hipSuccess) return hip_status(e, "permute");
   ExpertArgs a{T * k, H, E, F, w.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
-               static_cast<const bf16_t*>(w_down), w.offsets, w.tile_start, nullptr, nullptr, w.a};
+               static_cast<const bf16_t*>(w_down), w.offsets, w.tile_start, w.tile_desc, nullptr, nullptr, w.a};
   if (w.xp == nullptr) {
     a.xp = xb;
     a.xp_rows = w.row_token;
@@ -409,11 +415,11 @@ int moe_experts_fwd(const moe_experts_dims* d, const void* xp, const int32_t* co
     return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const ExpSaved sv = exp_saved_layout(d, saved);
-  hipError_t e = launch_offsets_from_counts(counts, d->E, d->rows, sv.offsets, sv.tile_start, s);
+  hipError_t e = launch_offsets_from_counts(counts, d->E, d->rows, sv.offsets, sv.tile_start, sv.tile_desc, s);
   if (e != hipSuccess) return hip_status(e, "offsets");
   ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
                static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
-               sv.g, sv.u, sv.a};
+               sv.tile_desc, sv.g, sv.u, sv.a};
   e = launch_gateup_fwd(a, s);
   if (e != hipSuccess) return hip_status(e, "gate/up");
   e = launch_down_fwd(a, static_cast<bf16_t*>(o), s);
@@ -434,7 +440,7 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
   const ExpSaved sv = exp_saved_layout(d, const_cast<void*>(saved));
   ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
                static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
-               sv.g, sv.u, sv.a};
+               sv.tile_desc, sv.g, sv.u, sv.a};
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   hipError_t e = launch_experts_bwd(a, static_cast<const bf16_t*>(d_o), w.dg, w.du, static_cast<bf16_t*>(dxp),
                                     dw_gate, dw_up, dw_down, (d->flags & MOE_F_DW_FP32) != 0, s);

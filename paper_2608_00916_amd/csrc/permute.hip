@@ -66,23 +66,37 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* tmp) {
   return incl - v;
 }
 
+// Row-tile table of the grouped products: expert e's rows split into 128-row
+// tiles numbered from tile_start[e]; tile i is (first row, e | rows << 8).
+__device__ __forceinline__ void write_tiles(int e, int off, int n, int toff, int2* __restrict__ tile_desc) {
+  for (int i = 0; i * 128 < n; ++i) tile_desc[toff + i] = make_int2(off + i * 128, e | (min(128, n - i * 128) << 8));
+}
+
 // One workgroup: counts[e], offsets = exclusive scan (E+1), tile_start of
-// 128-row tiles (E+1), and chunk_base[c][e] = offsets[e] + rows of expert e
-// in chunks before c.
+// 128-row tiles (E+1) and the tile table, and chunk_base[c][e] = rows of
+// expert e in chunks before c.  The chunk counts pass through LDS in batches,
+// so each batch costs one round of parallel loads.
+constexpr int kScanBatch = 32;
+
 __global__ __launch_bounds__(256) void k_perm_scan(const int32_t* __restrict__ chunk_counts, int nchunks,
                                                    int E, int32_t* __restrict__ chunk_base,
                                                    int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-                                                   int32_t* __restrict__ tile_start) {
+                                                   int32_t* __restrict__ tile_start, int2* __restrict__ tile_desc) {
   __shared__ int tmp[256];
+  __shared__ int cc[kScanBatch][MOE_MAX_EXPERTS];
   const int e = threadIdx.x;
   int running = 0;
-  if (e < E)
-    for (int c = 0; c < nchunks; ++c) {
-      const int64_t i = static_cast<int64_t>(c) * E + e;
-      const int v = chunk_counts[i];
-      chunk_base[i] = running;
-      running += v;
-    }
+  for (int c0 = 0; c0 < nchunks; c0 += kScanBatch) {
+    const int nb = min(kScanBatch, nchunks - c0);
+    for (int i = threadIdx.x; i < nb * E; i += 256) cc[i / E][i % E] = chunk_counts[static_cast<int64_t>(c0) * E + i];
+    __syncthreads();
+    if (e < E)
+      for (int c = 0; c < nb; ++c) {
+        chunk_base[static_cast<int64_t>(c0 + c) * E + e] = running;
+        running += cc[c][e];
+      }
+    __syncthreads();
+  }
   const int n = e < E ? running : 0;
   const int off = block_exclusive_scan(n, tmp);
   const int tiles = cdiv(n, 128);
@@ -91,7 +105,7 @@ __global__ __launch_bounds__(256) void k_perm_scan(const int32_t* __restrict__ c
     counts[e] = n;
     offsets[e] = off;
     tile_start[e] = toff;
-    for (int c = 0; c < nchunks; ++c) chunk_base[static_cast<int64_t>(c) * E + e] += off;
+    write_tiles(e, off, n, toff, tile_desc);
   }
   if (e == E - 1) {
     offsets[E] = off + n;
@@ -101,6 +115,7 @@ __global__ __launch_bounds__(256) void k_perm_scan(const int32_t* __restrict__ c
 
 __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restrict__ topk_idx, int T, int E,
                                                          int k, const int32_t* __restrict__ chunk_base,
+                                                         const int32_t* __restrict__ offsets,
                                                          int32_t* __restrict__ row_token,
                                                          int32_t* __restrict__ row_of) {
   __shared__ unsigned long long bits[MOE_MAX_EXPERTS][kWords];
@@ -119,7 +134,7 @@ __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restri
     }
     int rank = __popcll(bits[e][w] & below);
     for (int ww = 0; ww < w; ++ww) rank += __popcll(bits[e][ww]);
-    const int r = chunk_base[static_cast<int64_t>(chunk) * E + e] + rank;
+    const int r = offsets[e] + chunk_base[static_cast<int64_t>(chunk) * E + e] + rank;
     row_token[r] = t;
     row_of[p] = r;
   }
@@ -168,7 +183,8 @@ __global__ __launch_bounds__(256) void k_permute_rows(const bf16_t* __restrict__
 // Experts path: offsets from device counts, clamped to the row capacity.
 __global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __restrict__ counts, int E,
                                                              int rows, int32_t* __restrict__ offsets,
-                                                             int32_t* __restrict__ tile_start) {
+                                                             int32_t* __restrict__ tile_start,
+                                                             int2* __restrict__ tile_desc) {
   __shared__ int tmp[256];
   const int e = threadIdx.x;
   const int c = e < E ? max(0, counts[e]) : 0;
@@ -180,6 +196,7 @@ __global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __re
   if (e < E) {
     offsets[e] = lo;
     tile_start[e] = toff;
+    write_tiles(e, lo, n, toff, tile_desc);
   }
   if (e == E - 1) {
     offsets[E] = hi;
@@ -192,8 +209,8 @@ __global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __re
 int64_t permute_ws_ints(int T, int E) { return 2 * static_cast<int64_t>(cdiv(T, kChunk)) * E; }
 
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
-                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int32_t* row_token,
-                          int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
+                          int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
+                          int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
   const int nchunks = cdiv(T, kChunk);
   int32_t* chunk_counts = ws;
   int32_t* chunk_base = ws + static_cast<int64_t>(nchunks) * E;
@@ -205,12 +222,12 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
   {
     TraceScope trace_scope(K_PERM_SCAN, s);
     hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(256), 0, s, chunk_counts, nchunks, E, chunk_base, counts,
-                       offsets, tile_start);
+                       offsets, tile_start, tile_desc);
   }
   {
     TraceScope trace_scope(K_PERM_SCATTER, s);
     hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
-                       row_token, row_of);
+                       offsets, row_token, row_of);
   }
   if (xp == nullptr) return hipGetLastError();
   // a few waves per CU suffice: each token's row is read once and written k times
@@ -228,10 +245,11 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
 }
 
 hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, int32_t* offsets,
-                                      int32_t* tile_start, hipStream_t s) {
+                                      int32_t* tile_start, int2* tile_desc, hipStream_t s) {
   {
     TraceScope trace_scope(K_OFFSETS, s);
-    hipLaunchKernelGGL(k_offsets_from_counts, dim3(1), dim3(256), 0, s, counts, E, rows, offsets, tile_start);
+    hipLaunchKernelGGL(k_offsets_from_counts, dim3(1), dim3(256), 0, s, counts, E, rows, offsets, tile_start,
+                       tile_desc);
   }
   return hipGetLastError();
 }
