@@ -323,7 +323,9 @@ __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int 
   constexpr int kMfma = C::FM * C::FN;                                      // per slice
   constexpr int kWrites = LA::kPer + C::NB * LB::kPer;
   constexpr int kLoads = kWrites;
-  static_assert(kReads <= kMfma, "slice reads must fit between the MFMAs of a slice");
+  // Wide tiles alternate one MFMA with one read, write or load; small tiles
+  // (more of those than MFMAs) spread them evenly over the MFMAs.
+  constexpr bool kOneEach = kReads <= kMfma && kWrites + kLoads <= kMfma;
   // One K step on LDS stage `set`: MFMAs of both 32-deep slices, the refill of
   // the other stage from the other register set (step kt + 1, loaded two steps
   // ago) and the global loads of step kt + 3 into that register set.  Loads
@@ -344,26 +346,30 @@ __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int 
     store(Other{}, nxt);
     load(Other{}, kt + 3);
     __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);  // slice-0 reads
+    if constexpr (kOneEach) {
 #pragma unroll
-    for (int i = 0; i < kReads; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // slice-1 read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
+      for (int i = 0; i < kReads; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // slice-1 read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
 #pragma unroll
-    for (int i = 0; i < kWrites; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
-    }
+      for (int i = 0; i < kWrites; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // LDS write
+      }
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+      for (int i = 0; i < kLoads; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global load
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kWrites - kLoads, 0);
+    } else {
+      interleave<kMfma, kReads, 0x100, 0, 0x200>();                 // slice-0 MFMAs + slice-1 reads
+      interleave<kMfma, kWrites, 0x200, kLoads, 0x020>();           // slice-1 MFMAs + refill
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kWrites - kLoads, 0);
     lds_barrier();
   };
-  static_assert(kWrites + kLoads <= kMfma, "refill must fit between the MFMAs of a slice");
 
   load(S0{}, 0);
   load(S1{}, 1);

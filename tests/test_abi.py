@@ -135,7 +135,7 @@ def test_trace_api_without_launches():
     n = L.moe_trace_read(None, None, 0)
     assert n >= 17
     names = {L.moe_trace_name(i).decode() for i in range(n)}
-    assert {"gateup_fwd", "gateup_wgrad", "combine", "topk"} <= names
+    assert {"router_logits", "topk", "gateup_fwd", "gateup_wgrad", "combine", "router_dx"} <= names
     assert L.moe_trace_name(-1).decode() == ""
 
 
