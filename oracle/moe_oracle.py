@@ -15,8 +15,9 @@ dropless top-k MoE with SwiGLU experts, under these readings:
   expert index; slots are ordered by descending logit;
 * gates are the softmax over the k selected logits (equal to the full softmax
   renormalised over the selection);
-* no capacity limit, no dropped tokens, no auxiliary loss, no shared expert,
-  no router bias;
+* no capacity limit, no dropped tokens, no shared expert, no router bias;
+  by default no auxiliary loss; optionally (the paper is silent on it; see
+  router_aux_loss) a load-balancing loss and a z-loss on the router logits;
 * masked (padding) tokens are not routed: they get no rows, Y = 0, dX = 0;
 * rows are permuted expert-major and, within an expert, by ascending token;
 * gates multiply the expert outputs at combine time;
@@ -234,14 +235,79 @@ def unpermute_sum(dxp, row_of, T):
     return out
 
 
-def moe_backward(x, w_r, w_gate, w_up, w_down, fwd, dY):
-    """Whole block backward: dX, dW_r, dW_gate, dW_up, dW_down."""
+# ---------------------------------------------------------------- router losses
+def router_probs(z, mask=None):
+    """Full softmax over the experts of each token, and its log-normaliser
+    lse_t = log sum_e exp z[t,e].  Masked tokens: p = 0, lse = 0."""
+    m = np.max(z, axis=1, keepdims=True)
+    ez = np.exp(z - m)
+    s = np.sum(ez, axis=1, keepdims=True)
+    p = ez / s
+    lse = (m + np.log(s))[:, 0]
+    if mask is not None:
+        p = np.where(mask[:, None], p, 0.0)
+        lse = np.where(mask, lse, 0.0)
+    return p, lse
+
+
+def router_aux_loss(z, idx, aux_coef, z_coef, mask=None):
+    """Auxiliary router losses over the T_v valid tokens (the paper is silent
+    on them; these are the load-balancing loss of Switch/GShard-style MoE
+    training and the router z-loss):
+        L_aux = aux_coef * E * sum_e f_e P_e,
+            f_e = (routed slots of expert e) / (T_v k),  P_e = mean_t p[t,e];
+        L_z   = z_coef * mean_t lse_t^2.
+    Returns (L_aux, L_z)."""
+    T, E = z.shape
+    k = idx.shape[1]
+    valid = np.ones(T, dtype=bool) if mask is None else mask
+    Tv = int(valid.sum())
+    if Tv == 0:
+        return 0.0, 0.0
+    p, lse = router_probs(z, valid)
+    f = np.zeros(E)
+    for e in range(E):
+        f[e] = np.count_nonzero(idx[valid] == e) / (Tv * k)
+    P = p[valid].sum(axis=0) / Tv
+    l_aux = aux_coef * E * float(np.dot(f, P))
+    l_z = z_coef * float(np.sum(lse[valid] ** 2)) / Tv
+    return l_aux, l_z
+
+
+def router_aux_dz(z, idx, aux_coef, z_coef, mask=None):
+    """d(L_aux + L_z)/dz with the routing fractions f held constant (they
+    are piecewise constant in z):
+        dL_aux/dz[t,i] = aux_coef E / T_v * p[t,i] (f_i - sum_e f_e p[t,e]),
+        dL_z/dz[t,i]   = z_coef 2 / T_v * lse_t p[t,i];
+    zero on masked tokens."""
+    T, E = z.shape
+    k = idx.shape[1]
+    valid = np.ones(T, dtype=bool) if mask is None else mask
+    Tv = int(valid.sum())
+    dz = np.zeros((T, E))
+    if Tv == 0:
+        return dz
+    p, lse = router_probs(z, valid)
+    f = np.array([np.count_nonzero(idx[valid] == e) for e in range(E)]) / (Tv * k)
+    fp = p @ f
+    dz += aux_coef * E / Tv * p * (f[None, :] - fp[:, None])
+    dz += z_coef * 2.0 / Tv * lse[:, None] * p
+    dz[~valid] = 0.0
+    return dz
+
+
+def moe_backward(x, w_r, w_gate, w_up, w_down, fwd, dY, aux=None, mask=None):
+    """Whole block backward: dX, dW_r, dW_gate, dW_up, dW_down.  With
+    aux = (aux_coef, z_coef) the router losses' gradient joins dz (the
+    losses enter the objective with weight 1)."""
     E = w_r.shape[1]
     T = x.shape[0]
     dO, dg = combine_backward(dY, fwd["O"], fwd["gates"], fwd["row_of"])
     eb = experts_backward(fwd["xp"], fwd["offsets"], w_gate, w_up, w_down,
                           fwd["G"], fwd["U"], fwd["A"], dO)
     dz = router_backward(fwd["gates"], dg, fwd["idx"], E)
+    if aux is not None:
+        dz = dz + router_aux_dz(fwd["z"], fwd["idx"], aux[0], aux[1], mask)
     dw_r = x.T @ dz
     dx = unpermute_sum(eb["dxp"], fwd["row_of"], T) + dz @ w_r.T
     return dict(dx=dx, dw_r=dw_r, dw_gate=eb["dw_gate"], dw_up=eb["dw_up"],

@@ -264,6 +264,109 @@ def test_gradients_match_torch_autograd():
         np.testing.assert_allclose(b[on], t[n].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=n)
 
 
+# ------------------------------------------------------------ router losses
+def test_aux_loss_closed_forms():
+    """Equal logits: every P_e = 1/E, so L_aux = aux_coef * sum_e f_e = aux_coef
+    whatever the routing, and lse = ln E, so L_z = z_coef (ln E)^2.  Balanced
+    routing (f_e = 1/E): L_aux = aux_coef * sum_e P_e = aux_coef for any
+    logits."""
+    T, E, k = 24, 6, 2
+    z = np.zeros((T, E))
+    idx = O.select_topk(z, k)
+    l_aux, l_z = O.router_aux_loss(z, idx, 0.01, 0.001)
+    assert math.isclose(l_aux, 0.01, rel_tol=1e-14)
+    assert math.isclose(l_z, 0.001 * math.log(E) ** 2, rel_tol=1e-14)
+    # balanced: token t prefers experts 2t, 2t+1 (mod E): 24 tokens x 2 slots = 8 per expert
+    g = np.random.default_rng(3)
+    z = g.standard_normal((T, E)) * 0.1
+    for t in range(T):
+        z[t, (2 * t) % E] += 10.0
+        z[t, (2 * t + 1) % E] += 9.0
+    idx = O.select_topk(z, k)
+    counts = np.bincount(idx.ravel(), minlength=E)
+    assert np.all(counts == T * k // E)
+    l_aux, _ = O.router_aux_loss(z, idx, 0.3, 0.0)
+    assert math.isclose(l_aux, 0.3, rel_tol=1e-13)
+    # masked tokens count nowhere: masking half the tokens equals dropping them
+    mask = np.arange(T) % 2 == 0
+    a = O.router_aux_loss(z, idx, 0.3, 0.2, mask)
+    b = O.router_aux_loss(z[mask], idx[mask], 0.3, 0.2)
+    assert np.allclose(a, b, rtol=1e-14)
+
+
+def test_aux_dz_matches_finite_differences():
+    """The analytic gradient of L_aux + L_z against central differences of
+    the loss definition in z, routing held fixed (f is piecewise constant)."""
+    g = np.random.default_rng(21)
+    T, E, k = 40, 8, 3
+    z = g.standard_normal((T, E))
+    mask = g.random(T) > 0.2
+    idx = O.select_topk(z, k, mask)
+    dz = O.router_aux_dz(z, idx, 0.05, 0.02, mask)
+    assert np.all(dz[~mask] == 0)
+
+    def total(zz):
+        a, b = O.router_aux_loss(zz, idx, 0.05, 0.02, mask)
+        return a + b
+    eps = 1e-6
+    for _ in range(4):
+        v = g.standard_normal(z.shape)
+        fd = (total(z + eps * v) - total(z - eps * v)) / (2 * eps)
+        an = float(np.sum(dz * v))
+        assert abs(fd - an) <= 1e-8 * max(1.0, abs(an)), (fd, an)
+
+
+def test_aux_dz_matches_torch_autograd():
+    import torch
+    g = np.random.default_rng(22)
+    T, E, k = 50, 16, 4
+    z = g.standard_normal((T, E)) * 2.0
+    mask = g.random(T) > 0.3
+    idx = O.select_topk(z, k, mask)
+    Tv = int(mask.sum())
+    f = torch.zeros(E, dtype=torch.float64)
+    for e in range(E):
+        f[e] = float(np.count_nonzero(idx[mask] == e)) / (Tv * k)
+    zt = torch.tensor(z, requires_grad=True)
+    m = torch.from_numpy(mask)
+    p = torch.softmax(zt, dim=1)[m]
+    lse = torch.logsumexp(zt, dim=1)[m]
+    loss = 0.07 * E * torch.sum(f * p.mean(dim=0)) + 0.03 * torch.mean(lse ** 2)
+    loss.backward()
+    np.testing.assert_allclose(O.router_aux_dz(z, idx, 0.07, 0.03, mask), zt.grad.numpy(), rtol=1e-10,
+                               atol=1e-13)
+    a, b = O.router_aux_loss(z, idx, 0.07, 0.03, mask)
+    assert math.isclose(a + b, float(loss.detach()), rel_tol=1e-12)
+
+
+def test_block_gradients_with_aux_match_finite_differences():
+    """The block objective <Y, dY> + L_aux + L_z: its dW_r and dX from
+    moe_backward(aux=...) against central differences (routing tie-free)."""
+    x, w_r, w_g, w_u, w_d, dy, mask = _fd_setup()
+    k = FD_SHAPE["k"]
+    aux = (0.05, 0.01)
+    f0 = O.moe_forward(x, w_r, w_g, w_u, w_d, k, mask)
+
+    def loss(xx, wr):
+        f = O.moe_forward(xx, wr, w_g, w_u, w_d, k, mask)
+        assert np.array_equal(f["idx"], f0["idx"])
+        a, b = O.router_aux_loss(f["z"], f["idx"], aux[0], aux[1], mask)
+        return float(np.sum(dy * f["Y"])) + a + b
+
+    b = O.moe_backward(x, w_r, w_g, w_u, w_d, f0, dy, aux=aux, mask=mask)
+    g = np.random.default_rng(4)
+    eps = 1e-6
+    for _ in range(3):
+        v = g.standard_normal(w_r.shape)
+        fd = (loss(x, w_r + eps * v) - loss(x, w_r - eps * v)) / (2 * eps)
+        an = float(np.sum(b["dw_r"] * v))
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), ("w_r", fd, an)
+        v = g.standard_normal(x.shape)
+        fd = (loss(x + eps * v, w_r) - loss(x - eps * v, w_r)) / (2 * eps)
+        an = float(np.sum(b["dx"] * v))
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), ("x", fd, an)
+
+
 # ------------------------------------------------------------ workloads
 def test_workload_routing_statistics():
     """The Zipf workload: hottest expert about ten times the mean, four experts
