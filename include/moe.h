@@ -23,7 +23,8 @@
  *
  * The paper does not print these equations; the readings taken where it is
  * silent (selection precision, tie-break, gate placement, padding, dropless
- * routing, no auxiliary loss) are the ones stated above.
+ * routing, auxiliary router losses off unless asked for) are the ones stated
+ * above and at moe_dims.
  *
  * Conventions shared by every entry point
  *   - All tensors are row-major and live in device memory owned by the
@@ -52,7 +53,8 @@ extern "C" {
 
 /* return codes */
 #define MOE_OK 0
-#define MOE_ERR_ARG (-1)       /* null pointer, non-positive size, k not in [1, E], E too large */
+#define MOE_ERR_ARG (-1)       /* null pointer, non-positive size, k not in [1, E], E too large,
+                                * a router-loss coefficient negative or not finite */
 #define MOE_ERR_SHAPE (-2)     /* H or F not a multiple of 128, E not a multiple of 8 */
 #define MOE_ERR_ALIGN (-3)     /* a device pointer not 16-byte aligned */
 #define MOE_ERR_WORKSPACE (-4) /* workspace smaller than the size query returns */
@@ -72,10 +74,22 @@ extern "C" {
                             * without the flag */
 
 /* Sizes of the full block.  T tokens (T >= 1), hidden size H, E experts,
- * expert width F, top_k experts per token. */
+ * expert width F, top_k experts per token.
+ *
+ * Router losses (the paper is silent on them; 0 = off, the default):
+ *   aux_loss_coef  load-balancing loss  L_aux = aux_loss_coef * E * sum_e f_e P_e,
+ *                  f_e = rows of expert e / (T_v k), P_e = mean over valid
+ *                  tokens of the full softmax of the logits;
+ *   z_loss_coef    z-loss  L_z = z_loss_coef * mean over valid tokens of
+ *                  (log sum_e exp z[t,e])^2.
+ * With either non-zero, moe_fwd writes {L_aux, L_z} (moe_saved_view.router_loss)
+ * and moe_bwd adds their gradient (f held constant) to the router-logit
+ * gradient, i.e. the losses join the objective with weight 1.  Both must be
+ * finite and >= 0. */
 typedef struct moe_dims {
   int32_t T, H, E, F, top_k;
   uint32_t flags;
+  float aux_loss_coef, z_loss_coef;
 } moe_dims;
 
 /* Device pointers into a `saved` buffer filled by moe_fwd (see
@@ -94,6 +108,7 @@ typedef struct moe_saved_view {
   void* u;            /* [R_cap, F]  bf16 up projection U (NULL with MOE_F_RECOMPUTE) */
   void* a;            /* [R_cap, F]  bf16 SwiGLU activation A = silu(G) * U */
   void* o;            /* [R_cap, H]  bf16 expert outputs O (ungated) */
+  float* router_loss; /* [2]         {L_aux, L_z}, written when a router-loss coefficient is non-zero */
 } moe_saved_view;
 
 /* Bytes of the caller-owned `saved` buffer that carries routing and
@@ -142,7 +157,8 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
  * workspace, G and U are never stored, and the gate/up product reads its rows
  * of x through the permutation instead of a gathered copy (a copy is made in
  * the workspace only when T * H * 2 bytes exceed 2^31 - 1).  MOE_F_MASK as in
- * moe_fwd; MOE_F_DW_FP32 and MOE_F_RECOMPUTE are ignored.
+ * moe_fwd; MOE_F_DW_FP32, MOE_F_RECOMPUTE and the router-loss coefficients
+ * are ignored.
  *   x, w_r, w_gate, w_up, w_down, token_mask, y   as in moe_fwd
  *   ws    moe_infer_workspace_bytes(d) bytes of scratch
  */

@@ -27,10 +27,11 @@ __all__ = [
 ]
 
 
-def dims(T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False) -> MoeDims:
+def dims(T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False, aux_loss_coef=0.0,
+         z_loss_coef=0.0) -> MoeDims:
     flags = ((MOE_F_MASK if mask else 0) | (MOE_F_DW_FP32 if dw_fp32 else 0)
              | (MOE_F_RECOMPUTE if recompute else 0))
-    return MoeDims(T, H, E, F, top_k, flags)
+    return MoeDims(T, H, E, F, top_k, flags, aux_loss_coef, z_loss_coef)
 
 
 def experts_dims(rows, H, E, F, dw_fp32=False, recompute=False) -> MoeExpertsDims:
@@ -124,6 +125,7 @@ def moe_saved_views(d: MoeDims, saved: torch.Tensor) -> dict:
         u=_view(saved, v.u, bf, (R, F)),
         a=_view(saved, v.a, bf, (R, F)),
         o=_view(saved, v.o, bf, (R, H)),
+        router_loss=_view(saved, v.router_loss, f32, (2,)),
     )
 
 
@@ -188,8 +190,9 @@ class MoEBlock:
     """Caller-side buffers for one block shape: saved activations, workspaces
     and outputs, allocated once with torch on `device`."""
 
-    def __init__(self, T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False, device="cuda"):
-        self.d = dims(T, H, E, F, top_k, mask, dw_fp32, recompute)
+    def __init__(self, T, H, E, F, top_k, mask=False, dw_fp32=False, recompute=False, aux_loss_coef=0.0,
+                 z_loss_coef=0.0, device="cuda"):
+        self.d = dims(T, H, E, F, top_k, mask, dw_fp32, recompute, aux_loss_coef, z_loss_coef)
         nb = moe_saved_bytes(self.d)
         if nb == 0:
             raise MoeError(_lib.MOE_ERR_ARG, moe_last_error())

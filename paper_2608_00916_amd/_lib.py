@@ -35,13 +35,14 @@ EXPORTS = (
 
 class MoeDims(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("E", ctypes.c_int32),
-                ("F", ctypes.c_int32), ("top_k", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+                ("F", ctypes.c_int32), ("top_k", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("aux_loss_coef", ctypes.c_float), ("z_loss_coef", ctypes.c_float)]
 
 
 class MoeSavedView(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "logits", "topk_idx", "gates", "counts", "offsets", "row_token", "row_of",
-        "xp", "g", "u", "a", "o")]
+        "xp", "g", "u", "a", "o", "router_loss")]
 
 
 class MoeExpertsDims(ctypes.Structure):

@@ -65,15 +65,29 @@ __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, c
 //   dg_j      = <dY[t], O[r_j]>                              (fp32)
 //   dz_j      = g_j (dg_j - sum_j' g_j' dg_j')               (fp32, per slot)
 //   dz[t, :]  = dz_j at e = idx_j, else 0                    (bf16, all E)
-template <int KT>
-__global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ dy,
+// With the router losses (RouterLossGrad.on) dz[t, :] also takes, for a
+// valid token, their gradient with the routing fractions f held constant:
+//   aux_coef E / T_v  p_e (f_e - sum_e' f_e' p_e') + z_coef 2 / T_v  lse p_e,
+// p the full softmax of the token's fp32 logits, lse their log-normaliser,
+// f_e = counts[e] / R, T_v = R / k.
+struct RouterLossGrad {
+  const float* logits = nullptr;
+  const int32_t* counts = nullptr;
+  const int32_t* offsets = nullptr;
+  float aux_coef = 0.0f, z_coef = 0.0f;
+};
+
+constexpr int kMaxPerLane = MOE_MAX_EXPERTS / kWave;
+
+template <int KT, bool kAux>
+__device__ __forceinline__ void combine_bwd_body(const bf16_t* __restrict__ dy,
                                                      const bf16_t* __restrict__ o,
                                                      const float* __restrict__ gates,
                                                      const int32_t* __restrict__ topk_idx,
                                                      const int32_t* __restrict__ row_of, int T, int H,
                                                      int E, int k, bf16_t* __restrict__ d_o,
                                                      float* __restrict__ dg_out, float* __restrict__ dz_slot,
-                                                     bf16_t* __restrict__ dz) {
+                                                     bf16_t* __restrict__ dz, RouterLossGrad rl) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -125,9 +139,49 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ 
     dg_out[static_cast<int64_t>(t) * k + lane] = my_dg;
     dz_slot[static_cast<int64_t>(t) * k + lane] = my_dz;
   }
+  float extra[kMaxPerLane];
+#pragma unroll
+  for (int m = 0; m < kMaxPerLane; ++m) extra[m] = 0.0f;
+  if constexpr (kAux) {
+    if (rows[0] >= 0) {  // a valid token (slot 0 is routed)
+      const float* zr = rl.logits + static_cast<int64_t>(t) * E;
+      const int R = rl.offsets[E];
+      const float tv = static_cast<float>(R / k);
+      float zv[kMaxPerLane], f[kMaxPerLane];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < kMaxPerLane; ++m) {
+        const int e = lane + kWave * m;
+        zv[m] = e < E ? zr[e] : -INFINITY;
+        f[m] = e < E ? static_cast<float>(rl.counts[e]) / static_cast<float>(R) : 0.0f;
+        mx = fmaxf(mx, zv[m]);
+      }
+      mx = wave_max(mx);
+      float p[kMaxPerLane], s = 0.0f;
+#pragma unroll
+      for (int m = 0; m < kMaxPerLane; ++m) {
+        p[m] = lane + kWave * m < E ? expf(zv[m] - mx) : 0.0f;
+        s += p[m];
+      }
+      s = wave_sum(s);
+      float fp = 0.0f;
+#pragma unroll
+      for (int m = 0; m < kMaxPerLane; ++m) {
+        p[m] /= s;
+        fp += f[m] * p[m];
+      }
+      fp = wave_sum(fp);
+      const float lse = mx + logf(s);
+      const float ca = rl.aux_coef * static_cast<float>(E) / tv, cz = rl.z_coef * 2.0f / tv * lse;
+#pragma unroll
+      for (int m = 0; m < kMaxPerLane; ++m) extra[m] = ca * p[m] * (f[m] - fp) + cz * p[m];
+    }
+  }
   bf16_t* dzr = dz + static_cast<int64_t>(t) * E;
-  for (int e0 = 0; e0 < E; e0 += kWave) {
-    const int e = e0 + lane;
+#pragma unroll
+  for (int m = 0; m < kMaxPerLane; ++m) {
+    const int e = kWave * m + lane;
+    if (kWave * m >= E) break;
     float v = 0.0f;
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
@@ -135,9 +189,24 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ 
       const float dzj = __shfl(my_dz, j, kWave);
       if (ej == e) v = dzj;
     }
-    if (e < E) dzr[e] = f2bf(v);
+    if (e < E) dzr[e] = f2bf(v + extra[m]);
   }
 }
+
+#define MOE_COMBINE_BWD_ALIAS(NAME, AUX)                                                                     \
+  template <int KT>                                                                                          \
+  __global__ __launch_bounds__(256) void NAME(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ o,   \
+                                              const float* __restrict__ gates,                               \
+                                              const int32_t* __restrict__ topk_idx,                          \
+                                              const int32_t* __restrict__ row_of, int T, int H, int E, int k, \
+                                              bf16_t* __restrict__ d_o, float* __restrict__ dg,              \
+                                              float* __restrict__ dz_slot, bf16_t* __restrict__ dz,          \
+                                              RouterLossGrad rl) {                                           \
+    combine_bwd_body<KT, AUX>(dy, o, gates, topk_idx, row_of, T, H, E, k, d_o, dg, dz_slot, dz, rl);        \
+  }
+MOE_COMBINE_BWD_ALIAS(k_combine_bwd_noaux, false)
+MOE_COMBINE_BWD_ALIAS(k_combine_bwd_aux, true)
+#undef MOE_COMBINE_BWD_ALIAS
 
 }  // namespace
 
@@ -162,11 +231,26 @@ hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* ro
 
 hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
                               const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz, hipStream_t s) {
+                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz,
+                              const float* logits, const int32_t* counts, const int32_t* offsets,
+                              float aux_coef, float z_coef, hipStream_t s) {
+  RouterLossGrad rl;
+  const bool aux = aux_coef != 0.0f || z_coef != 0.0f;
+  if (aux) {
+    rl.logits = logits;
+    rl.counts = counts;
+    rl.offsets = offsets;
+    rl.aux_coef = aux_coef;
+    rl.z_coef = z_coef;
+  }
   {
     TraceScope trace_scope(K_COMBINE_BWD, s);
-    MOE_SLOT_DISPATCH(k_combine_bwd, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k, d_o,
-                      dg, dz_slot, dz);
+    if (aux)
+      MOE_SLOT_DISPATCH(k_combine_bwd_aux, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k, d_o,
+                        dg, dz_slot, dz, rl);
+    else
+      MOE_SLOT_DISPATCH(k_combine_bwd_noaux, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k,
+                        d_o, dg, dz_slot, dz, rl);
   }
   return hipGetLastError();
 }

@@ -53,9 +53,15 @@ hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, co
 
 // ---- routing (router.hip)
 // logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
+// With aux_ws (router_loss_ws_floats(T, E) floats) also the per-workgroup
+// partial sums of the router losses.
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
-                             int E, int k, float* logits, int32_t* topk_idx, float* gates,
+                             int E, int k, float* logits, int32_t* topk_idx, float* gates, float* aux_ws,
                              hipStream_t s);
+int64_t router_loss_ws_floats(int T, int E);
+// out[0..1] = {L_aux, L_z} from those partial sums and the routing counts.
+hipError_t launch_router_loss(const float* aux_ws, int T, int E, int k, const int32_t* counts,
+                              const int32_t* offsets, float aux_coef, float z_coef, float* out, hipStream_t s);
 
 // ---- permutation (permute.hip)
 // Workspace ints the permutation needs for T tokens and E experts.
@@ -76,10 +82,14 @@ hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, in
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s);
 // dO[row_of[t,j]] = g dY[t]; dg = <dY[t], O[row]>; dz per slot (fp32 [T,k])
-// and dense over E (bf16 [T,E]).
+// and dense over E (bf16 [T,E]).  With a non-zero router-loss coefficient the
+// dense dz also takes the router losses' gradient (from the fp32 logits, the
+// counts and offsets); dz per slot stays the gates' part.
 hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
                               const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz, hipStream_t s);
+                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz,
+                              const float* logits, const int32_t* counts, const int32_t* offsets,
+                              float aux_coef, float z_coef, hipStream_t s);
 
 // ---- router backward (router_bwd.hip)
 int dwr_splits(int T);
@@ -87,8 +97,10 @@ int dwr_splits(int T);
 hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, float* ws_f32,
                       void* dw_r, bool f32_out, hipStream_t s);
 // dX[t] = sum_j (dXp[row_of[t,j]] + dz_j W_r[:, idx_j]); w_rt is [E,H] scratch.
+// With dz_dense (bf16 [T,E]) the router term is dz_dense W_r^T instead, formed
+// in `dense` (fp32 [T,H] scratch) by an MFMA product.
 hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
                             const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
-                            bf16_t* w_rt, bf16_t* dx, hipStream_t s);
+                            bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s);
 
 }  // namespace moe

@@ -3,6 +3,7 @@
 // sequence of the forward and backward passes on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -63,8 +64,14 @@ int check_dims(const moe_dims* d) {
     return fail(MOE_ERR_ARG, "T*top_k=%lld too large", static_cast<long long>(d->T) * d->top_k);
   if (d->flags & ~(MOE_F_MASK | MOE_F_DW_FP32 | MOE_F_RECOMPUTE))
     return fail(MOE_ERR_ARG, "unknown flags 0x%x", d->flags);
+  if (!std::isfinite(d->aux_loss_coef) || !std::isfinite(d->z_loss_coef) || d->aux_loss_coef < 0.0f ||
+      d->z_loss_coef < 0.0f)
+    return fail(MOE_ERR_ARG, "router-loss coefficients must be finite and >= 0 (aux %g, z %g)",
+                static_cast<double>(d->aux_loss_coef), static_cast<double>(d->z_loss_coef));
   return MOE_OK;
 }
+
+bool router_losses(const moe_dims* d) { return d->aux_loss_coef != 0.0f || d->z_loss_coef != 0.0f; }
 
 int check_experts_dims(const moe_experts_dims* d) {
   if (d == nullptr) return fail(MOE_ERR_ARG, "dims is NULL");
@@ -94,6 +101,7 @@ struct Saved {
   int2* tile_desc;
   float* gates;
   bf16_t *xp, *g, *u, *a, *o;
+  float* router_loss;
   size_t bytes;
 };
 
@@ -116,17 +124,36 @@ Saved saved_layout(const moe_dims* d, void* base) {
   s.u = keep_gu ? c.take<bf16_t>(R * F) : nullptr;
   s.a = c.take<bf16_t>(R * F);
   s.o = c.take<bf16_t>(R * H);
+  s.router_loss = c.take<float>(2);
   s.bytes = c.off;
   return s;
 }
 
-size_t fwd_ws(const moe_dims* d) { return up(permute_ws_ints(d->T, d->E) * sizeof(int32_t)); }
+// ---- layout of the forward workspace: permutation scratch, and the router
+// losses' partial sums when they are on
+struct FwdWs {
+  int32_t* perm;
+  float* loss;
+  size_t bytes;
+};
+
+FwdWs fwd_layout(const moe_dims* d, void* base) {
+  Carve c(base);
+  FwdWs w;
+  w.perm = c.take<int32_t>(static_cast<size_t>(permute_ws_ints(d->T, d->E)));
+  w.loss = router_losses(d) ? c.take<float>(static_cast<size_t>(router_loss_ws_floats(d->T, d->E))) : nullptr;
+  w.bytes = c.off;
+  return w;
+}
+
+size_t fwd_ws(const moe_dims* d) { return fwd_layout(d, nullptr).bytes; }
 
 // ---- layout of the backward workspace
 struct BwdWs {
   bf16_t* d_o;  // also dXp once dO is dead
   bf16_t *dg, *du, *dz, *w_rt;
   float *dgate, *dz_slot, *dwr_part;
+  float* dense;  // dz W_r^T (fp32 [T,H]) when the router losses are on
   size_t bytes;
 };
 
@@ -142,6 +169,7 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
   w.dz_slot = c.take<float>(T * k);
   w.w_rt = c.take<bf16_t>(E * H);
   w.dwr_part = c.take<float>(static_cast<size_t>(dwr_splits(d->T)) * H * E);
+  w.dense = router_losses(d) ? c.take<float>(T * H) : nullptr;
   w.bytes = c.off;
   return w;
 }
@@ -277,6 +305,7 @@ int moe_saved_views(const moe_dims* d, void* saved, moe_saved_view* v) {
   v->u = s.u;
   v->a = s.a;
   v->o = s.o;
+  v->router_loss = s.router_loss;
   return ok();
 }
 
@@ -289,18 +318,23 @@ int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
     return rc;
   const bool masked = d->flags & MOE_F_MASK;
   if (masked && token_mask == nullptr) return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
-  if (ws_bytes < fwd_ws(d))
-    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, fwd_ws(d));
+  const FwdWs fw = fwd_layout(d, ws);
+  if (ws_bytes < fw.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, fw.bytes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const Saved sv = saved_layout(d, saved);
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, sv.logits, sv.topk_idx, sv.gates, s);
+                                   E, k, sv.logits, sv.topk_idx, sv.gates, fw.loss, s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
-                     sv.row_of, sv.xp, static_cast<int32_t*>(ws), s);
+                     sv.row_of, sv.xp, fw.perm, s);
   if (e != hipSuccess) return hip_status(e, "permute");
+  if (fw.loss != nullptr) {
+    e = launch_router_loss(fw.loss, T, E, k, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef,
+                           sv.router_loss, s);
+    if (e != hipSuccess) return hip_status(e, "router losses");
+  }
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
   e = launch_gateup_fwd(a, s);
@@ -326,7 +360,8 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bool f32 = d->flags & MOE_F_DW_FP32;
   hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
-                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, s);
+                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, sv.logits, sv.counts,
+                                    sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
@@ -336,7 +371,7 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   if (e != hipSuccess) return hip_status(e, "experts bwd");
   // dX right after dXp, while much of dXp is still in the last-level cache.
   e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
-                       w.w_rt, static_cast<bf16_t*>(dx), s);
+                       w.w_rt, static_cast<bf16_t*>(dx), w.dense != nullptr ? w.dz : nullptr, w.dense, s);
   if (e != hipSuccess) return hip_status(e, "dx");
   e = launch_experts_bwd_gateup_w(a, w.dg, w.du, dw_gate, dw_up, f32, s);
   if (e != hipSuccess) return hip_status(e, "experts bwd");
@@ -363,7 +398,7 @@ int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, w.logits, w.topk_idx, w.gates, s);
+                                   E, k, w.logits, w.topk_idx, w.gates, nullptr, s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.tile_desc, w.row_token, w.row_of,
                      w.xp, w.perm, s);
@@ -449,6 +484,6 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
 
 const char* moe_last_error(void) { return g_err; }
 
-int moe_version(void) { return 101; }
+int moe_version(void) { return 200; }
 
 }  // extern "C"

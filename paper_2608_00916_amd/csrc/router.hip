@@ -62,40 +62,18 @@ __device__ __forceinline__ float key_value(uint32_t key) {
 
 __device__ __forceinline__ int ballot_count(bool p) { return __popcll(__ballot(p)); }
 
-// Top-k of one token per wave; lane l holds experts e = l + 64 m, m < PL.
-// Selection: the k largest logits, ties to the lower expert, in slot order
-// (descending logit, then ascending expert).  Exact: a radix search for the
-// k-th largest order key (each wave-wide count is a ballot and a popcount),
-// then the keys equal to it are taken by lower expert index; an entry's slot
-// counts the selected keys that beat it, broadcast one by one.  Gates
+// Top-k of one token, held by a wave: lane l holds the logits of experts
+// e = l + 64 m, m < PL (key 0 and value 0 where e >= E).  Selection: the k
+// largest logits, ties to the lower expert, in slot order (descending logit,
+// then ascending expert).  Exact: a radix search for the k-th largest order
+// key (each wave-wide count is a ballot and a popcount), then the keys equal
+// to it are taken by lower expert index; an entry's slot counts the selected
+// keys that beat it, broadcast one by one.  Gates
 // g_j = exp(z_j - z_0) / sum_j' exp(z_j' - z_0).  Keys of absent experts are
-// 0, below every logit's key, so they never count.  Many waves per SIMD hide
-// the latency of the wave-wide counts.
+// 0, below every logit's key, so they never count.  Returns the largest logit.
 template <int PL>
-__global__ __launch_bounds__(256) void k_topk(const float* __restrict__ logits, const uint8_t* __restrict__ mask,
-                                              int T, int E, int k, int32_t* __restrict__ topk_idx,
-                                              float* __restrict__ gates) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  int32_t* idx_row = topk_idx + static_cast<int64_t>(t) * k;
-  float* g_row = gates + static_cast<int64_t>(t) * k;
-  if (mask != nullptr && mask[t] == 0) {
-    if (lane < k) {
-      idx_row[lane] = -1;
-      g_row[lane] = 0.0f;
-    }
-    return;
-  }
-  const float* z = logits + static_cast<int64_t>(t) * E;
-  uint32_t key[PL];
-  float val[PL];
-#pragma unroll
-  for (int m = 0; m < PL; ++m) {
-    const int e = lane + kWave * m;
-    val[m] = e < E ? z[e] : 0.0f;
-    key[m] = e < E ? order_key(val[m]) : 0u;
-  }
+__device__ __forceinline__ float topk_select(const float (&val)[PL], const uint32_t (&key)[PL], int k, int lane,
+                                             int32_t* __restrict__ idx_row, float* __restrict__ g_row) {
   uint32_t kth = 0u;  // largest P with #{key >= P} >= k
   for (int b = 31; b >= 0; --b) {
     const uint32_t cand = kth | (1u << b);
@@ -155,12 +133,118 @@ __global__ __launch_bounds__(256) void k_topk(const float* __restrict__ logits, 
       idx_row[slot[m]] = lane + kWave * m;
       g_row[slot[m]] = wm[m] / sum;
     }
+  return top;
+}
+
+// One wave per token: the top-k and gates; masked tokens get expert -1 and
+// gate 0.  With kAux the workgroup (4 tokens) also writes one row of partial
+// sums for the router losses: the full softmax p[t,e] of its valid tokens
+// summed over the 4 tokens in order, and in column E the sum of lse_t^2
+// (lse_t = log sum_e exp z[t,e]).  Many waves per SIMD hide the latency of
+// the wave-wide counts.
+template <int PL, bool kAux>
+__global__ __launch_bounds__(256) void k_topk(const float* __restrict__ logits, const uint8_t* __restrict__ mask,
+                                              int T, int E, int k, int32_t* __restrict__ topk_idx,
+                                              float* __restrict__ gates, float* __restrict__ aux_part) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int t = blockIdx.x * 4 + wv;
+  if (!kAux && t >= T) return;
+  const bool on = t < T && (mask == nullptr || mask[t] != 0);
+  float val[PL];
+  uint32_t key[PL];
+  if (on) {
+    const float* z = logits + static_cast<int64_t>(t) * E;
+#pragma unroll
+    for (int m = 0; m < PL; ++m) {
+      const int e = lane + kWave * m;
+      val[m] = e < E ? z[e] : 0.0f;
+      key[m] = e < E ? order_key(val[m]) : 0u;
+    }
+    topk_select<PL>(val, key, k, lane, topk_idx + static_cast<int64_t>(t) * k, gates + static_cast<int64_t>(t) * k);
+  } else if (t < T && lane < k) {
+    topk_idx[static_cast<int64_t>(t) * k + lane] = -1;
+    gates[static_cast<int64_t>(t) * k + lane] = 0.0f;
+  }
+  if constexpr (kAux) {
+    __shared__ float part[4][MOE_MAX_EXPERTS + 1];
+    float p[PL];
+    float lse = 0.0f;
+#pragma unroll
+    for (int m = 0; m < PL; ++m) p[m] = 0.0f;
+    if (on) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < PL; ++m)
+        if (lane + kWave * m < E) mx = fmaxf(mx, val[m]);
+      mx = wave_max(mx);
+      float s = 0.0f;
+#pragma unroll
+      for (int m = 0; m < PL; ++m) {
+        p[m] = lane + kWave * m < E ? expf(val[m] - mx) : 0.0f;
+        s += p[m];
+      }
+      s = wave_sum(s);
+#pragma unroll
+      for (int m = 0; m < PL; ++m) p[m] /= s;
+      lse = mx + logf(s);
+    }
+#pragma unroll
+    for (int m = 0; m < PL; ++m)
+      if (lane + kWave * m < E) part[wv][lane + kWave * m] = p[m];
+    if (lane == 0) part[wv][E] = lse * lse;
+    __syncthreads();
+    float* row = aux_part + static_cast<int64_t>(blockIdx.x) * (E + 1);
+    for (int c = threadIdx.x; c <= E; c += 256) row[c] = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
+  }
+}
+
+// Router-loss sums: col[c] = sum of column c over the partial rows (each
+// thread sums a fixed set of rows in order, then a fixed tree).
+__global__ __launch_bounds__(256) void k_router_loss_cols(const float* __restrict__ part, int nrows, int ncols,
+                                                          float* __restrict__ col) {
+  __shared__ float red[256];
+  const int c = blockIdx.x;
+  float s = 0.0f;
+  for (int r = threadIdx.x; r < nrows; r += 256) s += part[static_cast<int64_t>(r) * ncols + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) col[c] = red[0];
+}
+
+// {L_aux, L_z} from the column sums and the routing counts:
+//   L_aux = aux_coef E sum_e f_e P_e = aux_coef E sum_e counts_e col_e / (R T_v),
+//   L_z = z_coef col_E / T_v,  R = offsets[E] = T_v k routed rows.
+__global__ __launch_bounds__(256) void k_router_loss_final(const float* __restrict__ col,
+                                                           const int32_t* __restrict__ counts,
+                                                           const int32_t* __restrict__ offsets, int E, int k,
+                                                           float aux_coef, float z_coef, float* __restrict__ out) {
+  __shared__ float red[256];
+  float s = 0.0f;
+  for (int e = threadIdx.x; e < E; e += 256) s += static_cast<float>(counts[e]) * col[e];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int R = offsets[E];
+    const float tv = static_cast<float>(R / k);
+    out[0] = R > 0 ? aux_coef * static_cast<float>(E) * red[0] / (static_cast<float>(R) * tv) : 0.0f;
+    out[1] = R > 0 ? z_coef * col[E] / tv : 0.0f;
+  }
 }
 
 }  // namespace
 
+int64_t router_loss_ws_floats(int T, int E) { return static_cast<int64_t>(cdiv(T, 4)) * (E + 1) + E + 1; }
+
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
-                             int E, int k, float* logits, int32_t* topk_idx, float* gates,
+                             int E, int k, float* logits, int32_t* topk_idx, float* gates, float* aux_ws,
                              hipStream_t s) {
   {
     TraceScope trace_scope(K_ROUTER_LOGITS, s);
@@ -171,12 +255,30 @@ hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* 
     TraceScope trace_scope(K_TOPK, s);
     const dim3 grid(cdiv(T, 4)), block(256);
     // experts per lane: 1, 2 or 4 (E <= 256)
-    if (E <= kWave)
-      hipLaunchKernelGGL(k_topk<1>, grid, block, 0, s, logits, mask, T, E, k, topk_idx, gates);
-    else if (E <= 2 * kWave)
-      hipLaunchKernelGGL(k_topk<2>, grid, block, 0, s, logits, mask, T, E, k, topk_idx, gates);
-    else
-      hipLaunchKernelGGL(k_topk<4>, grid, block, 0, s, logits, mask, T, E, k, topk_idx, gates);
+#define MOE_TOPK(PL, AUX) \
+  hipLaunchKernelGGL((k_topk<PL, AUX>), grid, block, 0, s, logits, mask, T, E, k, topk_idx, gates, aux_ws)
+    const bool aux = aux_ws != nullptr;
+    if (E <= kWave) {
+      if (aux) MOE_TOPK(1, true); else MOE_TOPK(1, false);
+    } else if (E <= 2 * kWave) {
+      if (aux) MOE_TOPK(2, true); else MOE_TOPK(2, false);
+    } else {
+      if (aux) MOE_TOPK(4, true); else MOE_TOPK(4, false);
+    }
+#undef MOE_TOPK
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_router_loss(const float* aux_ws, int T, int E, int k, const int32_t* counts,
+                              const int32_t* offsets, float aux_coef, float z_coef, float* out, hipStream_t s) {
+  const int nrows = cdiv(T, 4);
+  float* col = const_cast<float*>(aux_ws) + static_cast<int64_t>(nrows) * (E + 1);
+  {
+    TraceScope trace_scope(K_ROUTER_LOSS, s);
+    hipLaunchKernelGGL(k_router_loss_cols, dim3(E + 1), dim3(256), 0, s, aux_ws, nrows, E + 1, col);
+    hipLaunchKernelGGL(k_router_loss_final, dim3(1), dim3(256), 0, s, col, counts, offsets, E, k, aux_coef, z_coef,
+                       out);
   }
   return hipGetLastError();
 }

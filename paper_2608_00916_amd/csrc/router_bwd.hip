@@ -76,11 +76,14 @@ __global__ __launch_bounds__(256) void k_transpose_wr(const bf16_t* __restrict__
 
 // dX[t] = sum_j ( dXp[row_of[t,j]] + dz_j W_r[:, idx_j] ): dz is non-zero on
 // the k selected experts only, so the router term is k scaled rows of W_r^T
-// (L2-resident).  One wave per token, 8 columns per lane per pass.
-template <int KT>
+// (L2-resident).  With kDense the router term is instead a precomputed row of
+// dz W_r^T (fp32 [T][H]; dz dense over E when the router losses are on).  One
+// wave per token, 8 columns per lane per pass.
+template <int KT, bool kDense>
 __global__ __launch_bounds__(256) void k_router_dx(const float* __restrict__ dz_slot,
                                                    const int32_t* __restrict__ topk_idx,
                                                    const bf16_t* __restrict__ w_rt,
+                                                   const float* __restrict__ dense,
                                                    const bf16_t* __restrict__ dxp,
                                                    const int32_t* __restrict__ row_of, int T, int H, int k,
                                                    bf16_t* __restrict__ dx) {
@@ -102,22 +105,63 @@ __global__ __launch_bounds__(256) void k_router_dx(const float* __restrict__ dz_
     for (int j = 0; j < KT; ++j) {
       const bool on = rows[j] >= 0;
       v[j] = on ? *reinterpret_cast<const uint4*>(dxp + static_cast<int64_t>(rows[j]) * H + c) : make_uint4(0, 0, 0, 0);
-      w[j] = on ? *reinterpret_cast<const uint4*>(w_rt + static_cast<int64_t>(ex[j]) * H + c) : make_uint4(0, 0, 0, 0);
+      if constexpr (!kDense)
+        w[j] = on ? *reinterpret_cast<const uint4*>(w_rt + static_cast<int64_t>(ex[j]) * H + c) : make_uint4(0, 0, 0, 0);
     }
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if constexpr (kDense) {
+      if (rows[0] >= 0) {  // a routed token: its dense router term
+        const float4 a = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c);
+        const float4 b = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c + 4);
+        acc[0] = a.x, acc[1] = a.y, acc[2] = a.z, acc[3] = a.w;
+        acc[4] = b.x, acc[5] = b.y, acc[6] = b.z, acc[7] = b.w;
+      }
+    }
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
       const uint32_t* pv = reinterpret_cast<const uint32_t*>(&v[j]);
       const uint32_t* pw = reinterpret_cast<const uint32_t*>(&w[j]);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += lo_bf(pv[q]) + dzs[j] * lo_bf(pw[q]);
-        acc[2 * q + 1] += hi_bf(pv[q]) + dzs[j] * hi_bf(pw[q]);
+        if constexpr (kDense) {
+          acc[2 * q] += lo_bf(pv[q]);
+          acc[2 * q + 1] += hi_bf(pv[q]);
+        } else {
+          acc[2 * q] += lo_bf(pv[q]) + dzs[j] * lo_bf(pw[q]);
+          acc[2 * q + 1] += hi_bf(pv[q]) + dzs[j] * hi_bf(pw[q]);
+        }
       }
     }
     *reinterpret_cast<uint4*>(dx + static_cast<int64_t>(t) * H + c) =
         make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
                    pack_bf16x2(acc[6], acc[7]));
+  }
+}
+
+// dense[T][H] = dz W_r^T (fp32): A(m = t, k = e) = dz[t][e] and
+// B(n = h, k = e) = W_r[h][e], both K-contiguous; grid (T/128, H/128).
+__global__ __launch_bounds__(RTile::kThreads) void k_router_dx_dense(const bf16_t* __restrict__ dz,
+                                                                   const bf16_t* __restrict__ w_r, int T, int H,
+                                                                   int E, float* __restrict__ dense) {
+  using C = RTile;
+  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
+  const int m0 = blockIdx.x * C::BM, n0 = blockIdx.y * C::BN;
+  f32x4 acc[C::FM][C::FN];
+  zero_acc<C>(acc);
+  const bf16_t* bs[1] = {w_r + static_cast<int64_t>(n0) * E};
+  gemm_mainloop<C, true, true>(dz + static_cast<int64_t>(m0) * E, E, min(C::BM, T - m0), bs, E, H - n0, E, smem,
+                               acc);
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int mi = 0; mi < C::FM; ++mi) {
+    const int t = m0 + frag_row<C>(mi, lane);
+    if (t >= T) continue;
+#pragma unroll
+    for (int ni = 0; ni < C::FN; ++ni) {
+      const f32x4 v = acc[mi][ni];
+      *reinterpret_cast<float4*>(dense + static_cast<int64_t>(t) * H + n0 + frag_col<C>(ni, lane)) =
+          make_float4(v[0], v[1], v[2], v[3]);
+    }
   }
 }
 
@@ -147,20 +191,35 @@ hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, fl
 
 hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
                             const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
-                            bf16_t* w_rt, bf16_t* dx, hipStream_t s) {
-  {
+                            bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s) {
+  const bool use_dense = dz_dense != nullptr;
+  if (use_dense) {
+    TraceScope trace_scope(K_ROUTER_DX_DENSE, s);
+    hipLaunchKernelGGL(k_router_dx_dense, dim3(cdiv(T, RTile::BM), H / RTile::BN), dim3(RTile::kThreads), 0, s,
+                       dz_dense, w_r, T, H, E, dense);
+  } else {
     TraceScope trace_scope(K_TRANSPOSE_WR, s);
     hipLaunchKernelGGL(k_transpose_wr, dim3(cdiv(H, 32), cdiv(E, 32)), dim3(256), 0, s, w_r, H, E, w_rt);
   }
   {
     TraceScope trace_scope(K_ROUTER_DX, s);
-    const dim3 grid(cdiv(T, 4));
-    if (k <= 1) hipLaunchKernelGGL(k_router_dx<1>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
-    else if (k <= 2) hipLaunchKernelGGL(k_router_dx<2>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
-    else if (k <= 4) hipLaunchKernelGGL(k_router_dx<4>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
-    else if (k <= 8) hipLaunchKernelGGL(k_router_dx<8>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
-    else if (k <= 16) hipLaunchKernelGGL(k_router_dx<16>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
-    else hipLaunchKernelGGL(k_router_dx<32>, grid, dim3(256), 0, s, dz_slot, topk_idx, w_rt, dxp, row_of, T, H, k, dx);
+    const dim3 grid(cdiv(T, 4)), block(256);
+#define MOE_RDX(KT)                                                                                              \
+  do {                                                                                                           \
+    if (use_dense)                                                                                               \
+      hipLaunchKernelGGL((k_router_dx<KT, true>), grid, block, 0, s, dz_slot, topk_idx, w_rt, dense, dxp, row_of, \
+                         T, H, k, dx);                                                                           \
+    else                                                                                                         \
+      hipLaunchKernelGGL((k_router_dx<KT, false>), grid, block, 0, s, dz_slot, topk_idx, w_rt, dense, dxp,       \
+                         row_of, T, H, k, dx);                                                                   \
+  } while (0)
+    if (k <= 1) MOE_RDX(1);
+    else if (k <= 2) MOE_RDX(2);
+    else if (k <= 4) MOE_RDX(4);
+    else if (k <= 8) MOE_RDX(8);
+    else if (k <= 16) MOE_RDX(16);
+    else MOE_RDX(32);
+#undef MOE_RDX
   }
   return hipGetLastError();
 }

@@ -29,6 +29,8 @@ enum KernelId {
   K_OFFSETS,
   K_TRANSPOSE_WR,
   K_GATEUP_RECOMPUTE,
+  K_ROUTER_LOSS,
+  K_ROUTER_DX_DENSE,
   K_NUM_KERNELS
 };
 

@@ -35,8 +35,8 @@ def test_library_exports_every_declared_function():
     assert set(names) == set(_lib.EXPORTS)
 
 
-def D(T=256, H=128, E=8, F=256, k=2, flags=0):
-    return _lib.MoeDims(T, H, E, F, k, flags)
+def D(T=256, H=128, E=8, F=256, k=2, flags=0, aux=0.0, zl=0.0):
+    return _lib.MoeDims(T, H, E, F, k, flags, aux, zl)
 
 
 def test_size_queries():
@@ -101,6 +101,9 @@ def bwd(d, **over):
     (D(F=200), _lib.MOE_ERR_SHAPE),
     (D(E=12), _lib.MOE_ERR_SHAPE),
     (D(flags=8), _lib.MOE_ERR_ARG),
+    (D(aux=-0.01), _lib.MOE_ERR_ARG),           # router-loss coefficients >= 0
+    (D(zl=float("nan")), _lib.MOE_ERR_ARG),
+    (D(aux=float("inf")), _lib.MOE_ERR_ARG),
 ])
 def test_bad_dims(dims, code):
     assert fwd(dims) == code
@@ -155,3 +158,16 @@ def test_recompute_flag_layout():
     full = _lib.MoeExpertsDims(1000, 256, 4, 128, 0)
     assert (L.moe_experts_saved_bytes(ctypes.byref(full)) - L.moe_experts_saved_bytes(ctypes.byref(ed))
             == 2 * 1000 * 128 * 2)
+
+
+def test_router_loss_workspaces():
+    """Router losses on: the forward workspace holds their partial sums and the
+    backward workspace the dense dz W_r^T term; the saved buffer is unchanged."""
+    L = _lib.lib()
+    d, da = D(), D(aux=0.01, zl=0.001)
+    assert L.moe_saved_bytes(ctypes.byref(d)) == L.moe_saved_bytes(ctypes.byref(da))
+    assert L.moe_fwd_workspace_bytes(ctypes.byref(da)) >= L.moe_fwd_workspace_bytes(ctypes.byref(d)) + 64 * 9 * 4
+    assert L.moe_bwd_workspace_bytes(ctypes.byref(da)) >= L.moe_bwd_workspace_bytes(ctypes.byref(d)) + 256 * 128 * 4
+    v = _lib.MoeSavedView()
+    assert L.moe_saved_views(ctypes.byref(da), 1 << 20, ctypes.byref(v)) == 0
+    assert v.router_loss is not None and v.router_loss % 256 == 0

@@ -165,3 +165,55 @@ def test_recompute_is_bit_identical():
     for n in a:
         if n not in ("g", "u"):
             assert np.array_equal(a[n], r[n]), n
+
+
+@pytest.mark.parametrize("case", ["tiny_masked", "max_E"])
+def test_router_losses(case):
+    """Load-balancing loss and z-loss on: the loss values against the oracle's
+    definition (fp32 on the GPU), dX and dW_r against the oracle's backward with
+    the losses' gradient, and the forward outputs unchanged bit for bit.  The
+    coefficients are large enough that the losses' gradient dominates dW_r."""
+    import torch
+    import paper_2608_00916_amd as moe
+    if case == "tiny_masked":
+        inp = workloads.block_inputs(T=333, H=256, E=16, k=2, F=128, seed=51)
+        inp["mask"] = (np.arange(333) % 7 != 2).astype(np.uint8)
+    else:
+        inp = workloads.block_inputs(T=200, H=128, E=256, k=8, F=128, seed=52)
+    # a small upstream gradient, so that the losses' gradient dominates dz
+    inp["dy"] = workloads.bf16_bits(O.widen_bf16(inp["dy"]) * 1e-3)
+    coefs = (0.5, 0.05)
+    d = inp["dims"]
+    mask = inp["mask"]
+    print(f"GPU block router losses {case} T={d['T']} E={d['E']} k={d['k']}", flush=True)
+    t = {n: dev_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    tm = None if mask is None else torch.from_numpy(mask.astype(np.uint8)).cuda()
+    outs = []
+    for c in ((0.0, 0.0), coefs):
+        blk = moe.MoEBlock(d["T"], d["H"], d["E"], d["F"], d["k"], mask=tm is not None, aux_loss_coef=c[0],
+                           z_loss_coef=c[1])
+        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
+        torch.cuda.synchronize()
+        outs.append(dict(y=host(blk.y), dx=host(blk.dx), dw_r=host(blk.dw_r), dw_gate=host(blk.dw_gate),
+                         loss=host(blk.views["router_loss"]), idx=host(blk.views["topk_idx"]),
+                         logits=host(blk.views["logits"]), gates=host(blk.views["gates"])))
+    base, g = outs
+    for n in ("y", "dw_gate"):
+        assert np.array_equal(base[n], g[n]), n
+    w = {n: O.widen_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    mb = None if mask is None else mask.astype(bool)
+    f = O.moe_forward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], d["k"], mb)
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"], d["k"], mb)
+    if flipped.any():
+        pytest.skip("a near tie chose a different expert set")
+    l_aux, l_z = O.router_aux_loss(f["z"], f["idx"], coefs[0], coefs[1], mb)
+    assert abs(g["loss"][0] - l_aux) <= 1e-4 * abs(l_aux), (g["loss"], l_aux)
+    assert abs(g["loss"][1] - l_z) <= 1e-4 * abs(l_z), (g["loss"], l_z)
+    b = O.moe_backward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, w["dy"], aux=coefs, mask=mb)
+    b0 = O.moe_backward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, w["dy"])
+    # the losses' gradient is the larger part of dW_r here
+    assert np.abs(b["dw_r"] - b0["dw_r"]).max() > 0.5 * np.abs(b0["dw_r"]).max()
+    assert_close("dx", g["dx"], b["dx"])
+    bound = router_grad_bound(f, w["dy"], w["x"])
+    assert_router_grad(g["dw_r"], b["dw_r"], bound)
