@@ -315,6 +315,98 @@ def moe_backward(x, w_r, w_gate, w_up, w_down, fwd, dY, aux=None, mask=None):
                 dG=eb["dG"], dU=eb["dU"])
 
 
+# ---------------------------------------------------------------- expert LoRA
+def lora_forward(x, w_r, w_gate, w_up, w_down, lora, k, mask=None):
+    """Block forward with rank-r adapters on every expert's gate/up (the fused
+    first projection) and down projections, base weights and router frozen
+    (§3, "LoRA target groups for MoE": adapters on the experts, router left
+    frozen).  lora = dict(scale, a1 [E,H,r], b1_gate [E,r,F], b1_up [E,r,F],
+    a2 [E,F,r], b2 [E,r,H]); per expert e the effective weights are
+        W_gate + scale a1 b1_gate,  W_up + scale a1 b1_up,  W_down + scale a2 b2,
+    computed through the rank-r intermediates P1 = scale Xp a1 and
+    P2 = scale A a2:
+        G = Xp W_gate + P1 b1_gate,  U = Xp W_up + P1 b1_up,  A = silu(G) U,
+        O = A W_down + P2 b2."""
+    E = w_r.shape[1]
+    s = lora["scale"]
+    z = router_logits(x, w_r)
+    idx = select_topk(z, k, mask)
+    g = topk_gates(z, idx)
+    counts, offsets, row_token, row_of = permutation(idx, E)
+    R = int(offsets[E])
+    xp = gather_rows(x, row_token, R)
+    F = w_gate.shape[2]
+    r = lora["a1"].shape[2]
+    G = np.zeros((R, F))
+    U = np.zeros((R, F))
+    A = np.zeros((R, F))
+    O = np.zeros((R, w_down.shape[2]))
+    P1 = np.zeros((R, r))
+    P2 = np.zeros((R, r))
+    for e in range(E):
+        lo, hi = offsets[e], offsets[e + 1]
+        if hi == lo:
+            continue
+        P1[lo:hi] = s * (xp[lo:hi] @ lora["a1"][e])
+        G[lo:hi] = xp[lo:hi] @ w_gate[e] + P1[lo:hi] @ lora["b1_gate"][e]
+        U[lo:hi] = xp[lo:hi] @ w_up[e] + P1[lo:hi] @ lora["b1_up"][e]
+        A[lo:hi] = silu(G[lo:hi]) * U[lo:hi]
+        P2[lo:hi] = s * (A[lo:hi] @ lora["a2"][e])
+        O[lo:hi] = A[lo:hi] @ w_down[e] + P2[lo:hi] @ lora["b2"][e]
+    Y = combine(O, g, row_of)
+    return dict(z=z, idx=idx, gates=g, counts=counts, offsets=offsets,
+                row_token=row_token, row_of=row_of, R=R, xp=xp, G=G, U=U, A=A,
+                O=O, Y=Y, P1=P1, P2=P2)
+
+
+def lora_backward(x, w_r, w_gate, w_up, w_down, lora, fwd, dY):
+    """Backward of lora_forward with the base weights and the router frozen:
+    dX and the adapter gradients.  Per expert, with Q2 = scale dO b2^T and
+    Q1 = scale (dG b1_gate^T + dU b1_up^T):
+        dA = dO W_down^T + Q2 a2^T,   d a2 = A^T Q2,   d b2 = P2^T dO,
+        dG, dU from dA (SwiGLU backward),
+        dXp = dG W_gate^T + dU W_up^T + Q1 a1^T,
+        d a1 = Xp^T Q1,  d b1_gate = P1^T dG,  d b1_up = P1^T dU;
+    dX = unpermute-sum of dXp + dz W_r^T (the router's input gradient; no
+    dW_r).  Experts with no rows get zero adapter gradients."""
+    E = w_r.shape[1]
+    T = x.shape[0]
+    s = lora["scale"]
+    dO, dg = combine_backward(dY, fwd["O"], fwd["gates"], fwd["row_of"])
+    R = fwd["R"]
+    xp, G, U, A = fwd["xp"], fwd["G"], fwd["U"], fwd["A"]
+    offsets = fwd["offsets"]
+    dxp = np.zeros_like(xp)
+    grads = {n: np.zeros_like(lora[n]) for n in ("a1", "b1_gate", "b1_up", "a2", "b2")}
+    r = lora["a1"].shape[2]
+    Q1 = np.zeros((R, r))
+    Q2 = np.zeros((R, r))
+    dG = np.zeros_like(G)
+    dU = np.zeros_like(U)
+    for e in range(E):
+        lo, hi = offsets[e], offsets[e + 1]
+        if hi == lo:
+            continue
+        Q2[lo:hi] = s * (dO[lo:hi] @ lora["b2"][e].T)
+        dA = dO[lo:hi] @ w_down[e].T + Q2[lo:hi] @ lora["a2"][e].T
+        grads["a2"][e] = A[lo:hi].T @ Q2[lo:hi]
+        grads["b2"][e] = fwd["P2"][lo:hi].T @ dO[lo:hi]
+        sg = sigmoid(G[lo:hi])
+        dG[lo:hi] = dA * U[lo:hi] * sg * (1.0 + G[lo:hi] * (1.0 - sg))
+        dU[lo:hi] = dA * silu(G[lo:hi])
+        Q1[lo:hi] = s * (dG[lo:hi] @ lora["b1_gate"][e].T + dU[lo:hi] @ lora["b1_up"][e].T)
+        dxp[lo:hi] = (dG[lo:hi] @ w_gate[e].T + dU[lo:hi] @ w_up[e].T
+                      + Q1[lo:hi] @ lora["a1"][e].T)
+        grads["a1"][e] = xp[lo:hi].T @ Q1[lo:hi]
+        grads["b1_gate"][e] = fwd["P1"][lo:hi].T @ dG[lo:hi]
+        grads["b1_up"][e] = fwd["P1"][lo:hi].T @ dU[lo:hi]
+    dz = router_backward(fwd["gates"], dg, fwd["idx"], E)
+    dx = unpermute_sum(dxp, fwd["row_of"], T) + dz @ w_r.T
+    out = dict(dx=dx, dO=dO, dG=dG, dU=dU, dxp=dxp, Q1=Q1, Q2=Q2, dz=dz)
+    out.update({"d" + n: v for n, v in grads.items()})
+    return out
+
+
 # ---------------------------------------------------------------- one EP rank
 def offsets_of(counts):
     offsets = np.zeros(len(counts) + 1, dtype=np.int64)

@@ -367,6 +367,96 @@ def test_block_gradients_with_aux_match_finite_differences():
         assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), ("x", fd, an)
 
 
+# ------------------------------------------------------------ expert LoRA
+def rand_lora(E, H, F, r, seed, scale=2.0, std=0.3):
+    g = np.random.default_rng(seed)
+    return dict(scale=scale, a1=g.standard_normal((E, H, r)) * std, b1_gate=g.standard_normal((E, r, F)) * std,
+                b1_up=g.standard_normal((E, r, F)) * std, a2=g.standard_normal((E, F, r)) * std,
+                b2=g.standard_normal((E, r, H)) * std)
+
+
+def test_lora_equals_merged_weights():
+    """LoRA is a low-rank update of the weights: the adapted forward equals
+    the plain forward with W + scale a b merged into every expert, and with
+    b1 = b2 = 0 (the usual initialisation) it equals the base forward."""
+    x, w_r, w_g, w_u, w_d, dy, mask = rand_block(70, 10, 6, 2, 7, seed=31, n_masked=5)
+    lo = rand_lora(6, 10, 7, 3, seed=32)
+    f = O.lora_forward(x, w_r, w_g, w_u, w_d, lo, 2, mask)
+    s = lo["scale"]
+    merged = O.moe_forward(x, w_r, w_g + s * lo["a1"] @ lo["b1_gate"], w_u + s * lo["a1"] @ lo["b1_up"],
+                           w_d + s * lo["a2"] @ lo["b2"], 2, mask)
+    for n in ("G", "U", "A", "O", "Y"):
+        np.testing.assert_allclose(f[n], merged[n], rtol=1e-12, atol=1e-12, err_msg=n)
+    zero = dict(lo, b1_gate=0 * lo["b1_gate"], b1_up=0 * lo["b1_up"], b2=0 * lo["b2"])
+    f0 = O.lora_forward(x, w_r, w_g, w_u, w_d, zero, 2, mask)
+    base = O.moe_forward(x, w_r, w_g, w_u, w_d, 2, mask)
+    np.testing.assert_array_equal(f0["Y"], base["Y"])
+
+
+def test_lora_gradients_match_finite_differences():
+    """Adapter gradients and dX of <Y, dY> against central differences
+    (routing tie-free), and dX equal to the merged-weight block's dX."""
+    x, w_r, w_g, w_u, w_d, dy, mask = _fd_setup()
+    k = FD_SHAPE["k"]
+    E, H, F = w_r.shape[1], x.shape[1], w_g.shape[2]
+    lo = rand_lora(E, H, F, 2, seed=33, scale=0.7)
+    f = O.lora_forward(x, w_r, w_g, w_u, w_d, lo, k, mask)
+    b = O.lora_backward(x, w_r, w_g, w_u, w_d, lo, f, dy)
+
+    def loss(xx, ll):
+        ff = O.lora_forward(xx, w_r, w_g, w_u, w_d, ll, k, mask)
+        assert np.array_equal(ff["idx"], f["idx"])
+        return float(np.sum(dy * ff["Y"]))
+    g = np.random.default_rng(5)
+    eps = 1e-6
+    for n in ("a1", "b1_gate", "b1_up", "a2", "b2"):
+        for _ in range(2):
+            v = g.standard_normal(lo[n].shape)
+            fd = (loss(x, dict(lo, **{n: lo[n] + eps * v})) - loss(x, dict(lo, **{n: lo[n] - eps * v}))) / (2 * eps)
+            an = float(np.sum(b["d" + n] * v))
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (n, fd, an)
+    v = g.standard_normal(x.shape)
+    fd = (loss(x + eps * v, lo) - loss(x - eps * v, lo)) / (2 * eps)
+    assert abs(fd - float(np.sum(b["dx"] * v))) <= 1e-6 * max(1.0, abs(fd))
+    s = lo["scale"]
+    wm = (w_g + s * lo["a1"] @ lo["b1_gate"], w_u + s * lo["a1"] @ lo["b1_up"], w_d + s * lo["a2"] @ lo["b2"])
+    fm = O.moe_forward(x, w_r, *wm, k, mask)
+    bm = O.moe_backward(x, w_r, *wm, fm, dy)
+    np.testing.assert_allclose(b["dx"], bm["dx"], rtol=1e-10, atol=1e-12)
+
+
+def test_lora_gradients_match_torch_autograd():
+    import torch
+    x, w_r, w_g, w_u, w_d, dy, mask = rand_block(50, 8, 5, 2, 6, seed=34, n_masked=4)
+    lo = rand_lora(5, 8, 6, 3, seed=35, scale=1.5)
+    k = 2
+    f = O.lora_forward(x, w_r, w_g, w_u, w_d, lo, k, mask)
+    b = O.lora_backward(x, w_r, w_g, w_u, w_d, lo, f, dy)
+    t = {n: torch.tensor(lo[n], requires_grad=True) for n in ("a1", "b1_gate", "b1_up", "a2", "b2")}
+    xt = torch.tensor(x, requires_grad=True)
+    valid = torch.from_numpy(mask)
+    idx = torch.from_numpy(np.where(f["idx"] < 0, 0, f["idx"]))
+    z = xt @ torch.from_numpy(w_r)
+    gates = torch.softmax(torch.gather(z, 1, idx), dim=1) * valid[:, None]
+    s = lo["scale"]
+    y = torch.zeros_like(xt)
+    for j in range(k):
+        for e in range(5):
+            sel = (idx[:, j] == e) & valid
+            if sel.any():
+                xs = xt[sel]
+                wg = torch.from_numpy(w_g[e]) + s * t["a1"][e] @ t["b1_gate"][e]
+                wu = torch.from_numpy(w_u[e]) + s * t["a1"][e] @ t["b1_up"][e]
+                wd = torch.from_numpy(w_d[e]) + s * t["a2"][e] @ t["b2"][e]
+                a = torch.nn.functional.silu(xs @ wg) * (xs @ wu)
+                y = y.index_add(0, sel.nonzero()[:, 0], gates[sel, j:j + 1] * (a @ wd))
+    np.testing.assert_allclose(y.detach().numpy(), f["Y"], rtol=1e-11, atol=1e-12)
+    (y * torch.from_numpy(dy)).sum().backward()
+    for n in t:
+        np.testing.assert_allclose(b["d" + n], t[n].grad.numpy(), rtol=1e-10, atol=1e-11, err_msg=n)
+    np.testing.assert_allclose(b["dx"], xt.grad.numpy(), rtol=1e-10, atol=1e-11)
+
+
 # ------------------------------------------------------------ workloads
 def test_workload_routing_statistics():
     """The Zipf workload: hottest expert about ten times the mean, four experts
