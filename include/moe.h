@@ -151,6 +151,50 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
             void* dx, void* dw_r, void* dw_gate, void* dw_up, void* dw_down, void* ws,
             size_t ws_bytes, void* stream);
 
+/* Expert LoRA (§3, "LoRA target groups for MoE"; §4.3): rank-r adapters on
+ * every expert's fused gate/up projection and its down projection, with the
+ * base expert weights and the router frozen.  Per expert e the effective
+ * weights are
+ *   W_gate[e] + scale a1[e] b1_gate[e],  W_up[e] + scale a1[e] b1_up[e],
+ *   W_down[e] + scale a2[e] b2[e],
+ * applied through the rank-r intermediates P1 = scale Xp a1 and
+ * P2 = scale A a2 (bf16, kept in the saved buffer after the block's own
+ * layout, so moe_saved_views applies to it unchanged).  The backward writes dX
+ * and the five adapter gradients (bf16, or fp32 with MOE_F_DW_FP32) and no base
+ * or router weight gradients; dX includes the router term (the router is
+ * frozen, not detached).  MOE_F_MASK, MOE_F_RECOMPUTE and the router-loss
+ * coefficients behave as in moe_fwd / moe_bwd. */
+typedef struct moe_lora {
+  int32_t rank;        /* r: 16, 32, 48 or 64 */
+  float scale;         /* multiplies every adapter product (alpha / r in the usual parametrisation) */
+  const void* a1;      /* [E, H, r] bf16 */
+  const void* b1_gate; /* [E, r, F] bf16 */
+  const void* b1_up;   /* [E, r, F] bf16 */
+  const void* a2;      /* [E, F, r] bf16 */
+  const void* b2;      /* [E, r, H] bf16 */
+} moe_lora;
+
+/* Bytes of the LoRA saved buffer and of the scratch either LoRA call needs
+ * (0 if d or rank is invalid). */
+size_t moe_lora_saved_bytes(const moe_dims* d, int32_t rank);
+size_t moe_lora_workspace_bytes(const moe_dims* d, int32_t rank);
+
+/* Forward with the adapters; arguments as moe_fwd plus `lora`. */
+int moe_lora_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+                 const void* w_up, const void* w_down, const moe_lora* lora,
+                 const uint8_t* token_mask, void* y, void* saved, void* ws, size_t ws_bytes,
+                 void* stream);
+
+/* Backward with the adapters, from the saved buffer of the matching
+ * moe_lora_fwd (same d, x, weights and adapters).
+ *   dy    [T, H] bf16;  dx  [T, H] bf16
+ *   da1 [E, H, r], db1_gate [E, r, F], db1_up [E, r, F], da2 [E, F, r],
+ *   db2 [E, r, H]: overwritten; zero for experts with no rows */
+int moe_lora_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+                 const void* w_up, const void* w_down, const moe_lora* lora, const void* dy,
+                 const void* saved, void* dx, void* da1, void* db1_gate, void* db1_up, void* da2,
+                 void* db2, void* ws, size_t ws_bytes, void* stream);
+
 /* Forward-only pass of the block for serving (reranking scores a batch of
  * query-passage pairs in one prefill pass, §4.2 "Inference throughput"): the Y of
  * moe_fwd, bit for bit, without a saved buffer.  Routing, A and O live in the

@@ -13,12 +13,13 @@ import torch
 
 from . import _lib
 from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_F_RECOMPUTE, MOE_MAX_EXPERTS, MOE_MAX_TOPK, MoeDims,
-                   MoeError, MoeExpertsDims, MoeExpertsSavedView, MoeSavedView, check, lib)
+                   MoeError, MoeExpertsDims, MoeExpertsSavedView, MoeLora, MoeSavedView, check, lib)
 
 __all__ = [
     "dims", "experts_dims", "moe_saved_bytes", "moe_fwd_workspace_bytes",
     "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_bwd",
     "moe_infer_workspace_bytes", "moe_infer", "MoEInfer",
+    "moe_lora_saved_bytes", "moe_lora_workspace_bytes", "moe_lora_fwd", "moe_lora_bwd", "lora_args", "MoELoRA",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes", "moe_experts_saved_views",
     "moe_experts_fwd", "moe_experts_bwd", "moe_last_error", "moe_version",
     "moe_trace_enable", "moe_trace_read", "MoEBlock", "MoEExperts", "MoeError", "MOE_F_MASK", "MOE_F_DW_FP32",
@@ -153,6 +154,34 @@ def moe_infer(d, x, w_r, w_gate, w_up, w_down, token_mask, y, ws, stream=None):
                           0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
 
 
+# ------------------------------------------------------------------ expert LoRA
+def lora_args(rank, scale, a1, b1_gate, b1_up, a2, b2) -> MoeLora:
+    """The adapter descriptor (device tensors stay owned by the caller)."""
+    return MoeLora(rank, scale, _p(a1), _p(b1_gate), _p(b1_up), _p(a2), _p(b2))
+
+
+def moe_lora_saved_bytes(d: MoeDims, rank: int) -> int:
+    return lib().moe_lora_saved_bytes(ctypes.byref(d), rank)
+
+
+def moe_lora_workspace_bytes(d: MoeDims, rank: int) -> int:
+    return lib().moe_lora_workspace_bytes(ctypes.byref(d), rank)
+
+
+def moe_lora_fwd(d, x, w_r, w_gate, w_up, w_down, lora: MoeLora, token_mask, y, saved, ws, stream=None):
+    check(lib().moe_lora_fwd(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
+                             ctypes.byref(lora), _p(token_mask), _p(y), _p(saved), _p(ws),
+                             0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
+def moe_lora_bwd(d, x, w_r, w_gate, w_up, w_down, lora: MoeLora, dy, saved, dx, da1, db1_gate, db1_up, da2, db2,
+                 ws, stream=None):
+    check(lib().moe_lora_bwd(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
+                             ctypes.byref(lora), _p(dy), _p(saved), _p(dx), _p(da1), _p(db1_gate), _p(db1_up),
+                             _p(da2), _p(db2), _p(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                             _s(stream)))
+
+
 # ------------------------------------------------------------------ experts only
 def moe_experts_saved_bytes(d: MoeExpertsDims) -> int:
     return lib().moe_experts_saved_bytes(ctypes.byref(d))
@@ -261,3 +290,37 @@ class MoEInfer:
     def forward(self, x, w_r, w_gate, w_up, w_down, token_mask=None, stream=None):
         moe_infer(self.d, x, w_r, w_gate, w_up, w_down, token_mask, self.y, self.ws, stream)
         return self.y
+
+
+class MoELoRA:
+    """Caller-side buffers of the block with rank-r expert adapters: saved
+    activations, workspace, dX and the adapter gradients."""
+
+    def __init__(self, T, H, E, F, top_k, rank, mask=False, dw_fp32=False, recompute=False, aux_loss_coef=0.0,
+                 z_loss_coef=0.0, device="cuda"):
+        self.d = dims(T, H, E, F, top_k, mask, dw_fp32, recompute, aux_loss_coef, z_loss_coef)
+        self.rank = rank
+        nb = moe_lora_saved_bytes(self.d, rank)
+        if nb == 0:
+            raise MoeError(_lib.MOE_ERR_ARG, "invalid dims or LoRA rank")
+        dev = torch.device(device)
+        self.saved = torch.empty(nb, dtype=torch.uint8, device=dev)
+        self.ws = torch.empty(moe_lora_workspace_bytes(self.d, rank), dtype=torch.uint8, device=dev)
+        wdt = torch.float32 if dw_fp32 else torch.bfloat16
+        self.y = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        self.dx = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        self.da1 = torch.empty((E, H, rank), dtype=wdt, device=dev)
+        self.db1_gate = torch.empty((E, rank, F), dtype=wdt, device=dev)
+        self.db1_up = torch.empty((E, rank, F), dtype=wdt, device=dev)
+        self.da2 = torch.empty((E, F, rank), dtype=wdt, device=dev)
+        self.db2 = torch.empty((E, rank, H), dtype=wdt, device=dev)
+        self.views = moe_saved_views(self.d, self.saved)
+
+    def forward(self, x, w_r, w_gate, w_up, w_down, lora: MoeLora, token_mask=None, stream=None):
+        moe_lora_fwd(self.d, x, w_r, w_gate, w_up, w_down, lora, token_mask, self.y, self.saved, self.ws, stream)
+        return self.y
+
+    def backward(self, x, w_r, w_gate, w_up, w_down, lora: MoeLora, dy, stream=None):
+        moe_lora_bwd(self.d, x, w_r, w_gate, w_up, w_down, lora, dy, self.saved, self.dx, self.da1, self.db1_gate,
+                     self.db1_up, self.da2, self.db2, self.ws, stream)
+        return self.dx, self.da1, self.db1_gate, self.db1_up, self.da2, self.db2

@@ -26,6 +26,7 @@ MOE_F_RECOMPUTE = 4
 EXPORTS = (
     "moe_saved_bytes", "moe_fwd_workspace_bytes", "moe_bwd_workspace_bytes",
     "moe_saved_views", "moe_fwd", "moe_bwd", "moe_infer_workspace_bytes", "moe_infer",
+    "moe_lora_saved_bytes", "moe_lora_workspace_bytes", "moe_lora_fwd", "moe_lora_bwd",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes",
     "moe_experts_saved_views", "moe_experts_fwd", "moe_experts_bwd",
     "moe_trace_enable", "moe_trace_read", "moe_trace_name",
@@ -43,6 +44,12 @@ class MoeSavedView(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "logits", "topk_idx", "gates", "counts", "offsets", "row_token", "row_of",
         "xp", "g", "u", "a", "o", "router_loss")]
+
+
+class MoeLora(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("a1", ctypes.c_void_p), ("b1_gate", ctypes.c_void_p), ("b1_up", ctypes.c_void_p),
+                ("a2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
 
 
 class MoeExpertsDims(ctypes.Structure):
@@ -85,6 +92,11 @@ def lib() -> ctypes.CDLL:
         "moe_fwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, S, P]),
         "moe_bwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, P, P, P, P, S, P]),
         "moe_infer_workspace_bytes": (S, [D]),
+        "moe_lora_saved_bytes": (S, [D, ctypes.c_int32]),
+        "moe_lora_workspace_bytes": (S, [D, ctypes.c_int32]),
+        "moe_lora_fwd": (ctypes.c_int, [D, P, P, P, P, P, ctypes.POINTER(MoeLora), P, P, P, P, S, P]),
+        "moe_lora_bwd": (ctypes.c_int, [D, P, P, P, P, P, ctypes.POINTER(MoeLora), P, P, P, P, P, P, P, P, P, S,
+                                        P]),
         "moe_infer": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, S, P]),
         "moe_experts_saved_bytes": (S, [ED]),
         "moe_experts_workspace_bytes": (S, [ED]),

@@ -53,13 +53,67 @@ __device__ __forceinline__ void for_each_grouped_tile(const int32_t* tile_start,
   }
 }
 
+// A rank-r adapter term of a grouped product, one more K segment (K = r):
+// A operand `a` [rows][rank] (bf16, K-contiguous), per-expert B operands b0
+// (and b1 for gate/up), whose layout each kernel states.
+struct LoraSeg {
+  const bf16_t* a = nullptr;
+  const bf16_t* b0 = nullptr;
+  const bf16_t* b1 = nullptr;
+  int rank = 0;
+};
+
+// Rank-r intermediates of the adapters, row-grouped like the expert products:
+//   out[r][q] = scale * sum_s X_s[r][:] W_s[e](:, q),  q < rank (16 per tile)
+// with X_s K-contiguous ([rows][K], ld ldx) and W_s per expert (e * estride):
+// MN-contiguous [K][rank] (the a matrices) or, with B_KC, K-contiguous rows q
+// of length K ([rank][K], the b matrices).  NSEG = 2 sums two segments (dG with
+// b1_gate and dU with b1_up).  2 waves of 64 x 16.
+using LoraRows = Tile<128, 16, 1, 2, 1>;
+template <bool B_KC, int NSEG>
+__global__ __launch_bounds__(LoraRows::kThreads) void k_lora_rows(
+    const bf16_t* __restrict__ x0, const bf16_t* __restrict__ x1, int64_t ldx, const bf16_t* __restrict__ w0,
+    const bf16_t* __restrict__ w1, int64_t estride, int K, const int32_t* __restrict__ tile_start,
+    const int2* __restrict__ tile_desc, int E, int rank, float scale, bf16_t* __restrict__ out) {
+  using C = LoraRows;
+  static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
+  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
+  for_each_grouped_tile(tile_start, tile_desc, E, rank / C::BN, [&](const MTile& t) {
+    f32x4 acc[C::FM][C::FN];
+    zero_acc<C>(acc);
+    const int q0 = t.nt * C::BN;
+    const int64_t wofs = static_cast<int64_t>(t.e) * estride + (B_KC ? static_cast<int64_t>(q0) * K : q0);
+    const int64_t ldw = B_KC ? K : rank;
+    const bf16_t* b0[1] = {w0 + wofs};
+    gemm_mainloop<C, true, B_KC>(x0 + static_cast<int64_t>(t.m0) * ldx, ldx, t.m_lim, b0, ldw, C::BN, K, smem, acc);
+    if constexpr (NSEG == 2) {
+      const bf16_t* b1[1] = {w1 + wofs};
+      gemm_mainloop<C, true, B_KC>(x1 + static_cast<int64_t>(t.m0) * ldx, ldx, t.m_lim, b1, ldw, C::BN, K, smem,
+                                   acc);
+    }
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int mi = 0; mi < C::FM; ++mi) {
+      const int r = frag_row<C>(mi, lane);
+      if (r >= t.m_lim) continue;
+      f32x4 v = acc[mi][0];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] *= scale;
+      *reinterpret_cast<uint2*>(out + static_cast<int64_t>(t.m0 + r) * rank + q0 + frag_col<C>(0, lane)) =
+          pack4_bf16(v);
+    }
+  });
+}
+
 // G = Xp W_gate[e], U = Xp W_up[e], A = silu(G) * U  (K = H, N = F).
 // The B tile holds 128 columns of W_gate next to the same 128 of W_up.
 // G and U are stored when g_out is non-null, A when a_out is.  With xp_rows
 // non-null, row r of the product is row xp_rows[r] of xp (the gather read
 // through the permutation; xp_bytes bounds xp).
+// With kLora the adapters' rank-r term joins as one more K segment:
+// [G | U] += P1 [b1_gate | b1_up][e] (P1 = scale Xp a1, [rows][r]).
 using GateUpFwd = Tile<128, 256, 2, 2, 4>;
-template <bool kRows>
+template <bool kRows, bool kLora>
 __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t* __restrict__ xp,
                                                          const int32_t* __restrict__ xp_rows,
                                                          int64_t xp_bytes,
@@ -69,7 +123,7 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
                                                          const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
                                                          int H, int F, bf16_t* __restrict__ g_out,
                                                          bf16_t* __restrict__ u_out,
-                                                         bf16_t* __restrict__ a_out) {
+                                                         bf16_t* __restrict__ a_out, LoraSeg lo) {
   using C = GateUpFwd;
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
@@ -84,6 +138,12 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
     else
       gemm_mainloop<C, true, false>(xp + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, F, F - n0, H, smem,
                                     acc);
+    if constexpr (kLora) {  // b1 is [E][r][F]: MN-contiguous like W_gate
+      const int64_t lofs = static_cast<int64_t>(t.e) * lo.rank * F + n0;
+      const bf16_t* bl[2] = {lo.b0 + lofs, lo.b1 + lofs};
+      gemm_mainloop<C, true, false>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, F, F - n0,
+                                    lo.rank, smem, acc);
+    }
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -107,13 +167,14 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
   });
 }
 
-// O = A W_down[e]  (K = F, N = H).
-template <class C>
+// O = A W_down[e]  (K = F, N = H); with kLora also O += P2 b2[e]
+// (P2 = scale A a2, [rows][r]; b2 [E][r][H] MN-contiguous).
+template <class C, bool kLora>
 __global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restrict__ act,
                                                        const bf16_t* __restrict__ w_down,
                                                        const int32_t* __restrict__ offsets,
                                                        const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
-                                                       int H, int F, bf16_t* __restrict__ o_out) {
+                                                       int H, int F, bf16_t* __restrict__ o_out, LoraSeg lo) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
   for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
@@ -123,6 +184,11 @@ __global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restri
     const bf16_t* bs[1] = {w_down + static_cast<int64_t>(t.e) * F * H + n0};
     gemm_mainloop<C, true, false>(act + static_cast<int64_t>(t.m0) * F, F, t.m_lim, bs, H, H - n0, F, smem,
                                   acc);
+    if constexpr (kLora) {
+      const bf16_t* bl[1] = {lo.b0 + static_cast<int64_t>(t.e) * lo.rank * H + n0};
+      gemm_mainloop<C, true, false>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, H, H - n0,
+                                    lo.rank, smem, acc);
+    }
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -141,12 +207,14 @@ __global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restri
 // dG and dU may overwrite G and U in place: each lane reads an element of G
 // and U before it writes the same element of dG and dU, and nothing else
 // reads them.
-template <class C>
+// With kLora dA also takes Q2 a2[e]^T (Q2 = scale dO b2^T, [rows][r]; a2
+// [E][F][r]: K-contiguous rows of the B tile).
+template <class C, bool kLora>
 __global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
     const bf16_t* __restrict__ d_o, const bf16_t* __restrict__ w_down, const bf16_t* g_in,
     const bf16_t* u_in, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* dg_out,
-    bf16_t* du_out) {
+    bf16_t* du_out, LoraSeg lo) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
   for_each_grouped_tile(tile_start, tile_desc, E, F / C::BN, [&](const MTile& t) {
@@ -157,6 +225,11 @@ __global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
     const bf16_t* bs[1] = {w_down + static_cast<int64_t>(t.e) * F * H + static_cast<int64_t>(n0) * H};
     gemm_mainloop<C, true, true>(d_o + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, H, F - n0, H, smem,
                                  acc);
+    if constexpr (kLora) {
+      const bf16_t* bl[1] = {lo.b0 + (static_cast<int64_t>(t.e) * F + n0) * lo.rank};
+      gemm_mainloop<C, true, true>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, lo.rank,
+                                   F - n0, lo.rank, smem, acc);
+    }
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -185,12 +258,15 @@ __global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
   });
 }
 
-// dXp = dG W_gate[e]^T + dU W_up[e]^T  (K = 2F in two segments, N = H).
-template <class C>
+// dXp = dG W_gate[e]^T + dU W_up[e]^T  (K = 2F in two segments, N = H); with
+// kLora a third segment Q1 a1[e]^T (Q1 = scale (dG b1_gate^T + dU b1_up^T),
+// [rows][r]; a1 [E][H][r]: K-contiguous rows of the B tile).
+template <class C, bool kLora>
 __global__ __launch_bounds__(C::kThreads) void k_gateup_dgrad(
     const bf16_t* __restrict__ dg_in, const bf16_t* __restrict__ du_in, const bf16_t* __restrict__ w_gate,
     const bf16_t* __restrict__ w_up, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* __restrict__ dxp_out) {
+    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* __restrict__ dxp_out,
+    LoraSeg lo) {
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
   for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
@@ -204,6 +280,11 @@ __global__ __launch_bounds__(C::kThreads) void k_gateup_dgrad(
     gemm_mainloop<C, true, true>(dg_in + aofs, F, t.m_lim, bg, F, H - n0, F, smem, acc);
     const bf16_t* bu[1] = {w_up + wofs};
     gemm_mainloop<C, true, true>(du_in + aofs, F, t.m_lim, bu, F, H - n0, F, smem, acc);
+    if constexpr (kLora) {
+      const bf16_t* bl[1] = {lo.b0 + (static_cast<int64_t>(t.e) * H + n0) * lo.rank};
+      gemm_mainloop<C, true, true>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, lo.rank,
+                                   H - n0, lo.rank, smem, acc);
+    }
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -320,6 +401,63 @@ struct GateUpWgradJobs {
   }
 };
 
+// Adapter weight gradients: out[e] = X_e^T Y_e with X [rows][M] (ld ldx) and
+// Y [rows][rank], K = rows of expert e, stored [E][M][rank] or, with trans,
+// [E][rank][M] (the b matrices): d a1 = Xp^T Q1, d a2 = A^T Q2,
+// d b2 = P2^T dO, d b1 = P1^T dG / dU.  Experts with no rows: zeros.
+using LoraW = Tile<128, 16, 1, 2, 1>;
+template <bool F32>
+struct LoraWgradJobs {
+  using C = LoraW;
+  const int32_t* offsets;
+  const bf16_t* x;
+  int64_t ldx;
+  int M;
+  const bf16_t* y;
+  int E, rank;
+  bool trans;
+  void* out;
+  __device__ bool get(int i, Job<C>& j) const {
+    const int nm = M / C::BM, nq = rank / C::BN;
+    const int logical = xcd_tile(blockIdx.x, gridDim.x) + i * gridDim.x;
+    if (logical >= E * nm * nq) return false;
+    const int e = logical / (nm * nq);
+    const int rem = logical - e * nm * nq;
+    const int r0 = offsets[e];
+    j.m0 = (rem / nq) * C::BM;
+    j.n0 = (rem % nq) * C::BN;
+    j.a = x + static_cast<int64_t>(r0) * ldx + j.m0;
+    j.lda = ldx;
+    j.m_lim = C::BM;
+    j.b[0] = y + static_cast<int64_t>(r0) * rank + j.n0;
+    j.ldb = rank;
+    j.n_lim = C::BN;
+    j.K = offsets[e + 1] - r0;
+    j.chain = false;
+    j.e = e;
+    return true;
+  }
+  __device__ void epilogue(const Job<C>& j, f32x4 (&acc)[C::FM][C::FN]) const {
+    const int lane = threadIdx.x & 63;
+    const int64_t obase = static_cast<int64_t>(j.e) * M * rank;
+#pragma unroll
+    for (int mi = 0; mi < C::FM; ++mi) {
+      const int m = j.m0 + frag_row<C>(mi, lane);
+      const int q = j.n0 + frag_col<C>(0, lane);
+      if (!trans) {
+        store4<F32>(out, obase + static_cast<int64_t>(m) * rank + q, acc[mi][0]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t o = obase + static_cast<int64_t>(q + i) * M + m;
+          if constexpr (F32) static_cast<float*>(out)[o] = acc[mi][0][i];
+          else static_cast<bf16_t*>(out)[o] = f2bf(acc[mi][0][i]);
+        }
+      }
+    }
+  }
+};
+
 // One persistent kernel for every product: the job provider decides.
 template <class P, bool A_KC, bool B_KC>
 __global__ __launch_bounds__(P::C::kThreads) void k_stream(P prov) {
@@ -383,32 +521,54 @@ void run_stream(const P& prov, int64_t max_jobs, int kid, hipStream_t s) {
 
 template <class C>
 void down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
-  auto k = k_down_fwd<C>;
+  const bool lora = a.lora.rank > 0;
+  auto k = lora ? k_down_fwd<C, true> : k_down_fwd<C, false>;
+  LoraSeg lo;
+  if (lora) {
+    lo.a = a.lora.p2;
+    lo.b0 = a.lora.b2;
+    lo.rank = a.lora.rank;
+  }
   const int grid =
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_DOWN_FWD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.act, a.w_down, a.offsets, a.tile_start, a.tile_desc, a.E,
-                     a.H, a.F, o);
+                     a.H, a.F, o, lo);
 }
 
 template <class C>
-void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, hipStream_t s) {
-  auto k = k_down_dgrad_swiglu<C>;
+void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, const bf16_t* q2, hipStream_t s) {
+  const bool lora = q2 != nullptr;
+  auto k = lora ? k_down_dgrad_swiglu<C, true> : k_down_dgrad_swiglu<C, false>;
+  LoraSeg lo;
+  if (lora) {
+    lo.a = q2;
+    lo.b0 = a.lora.a2;
+    lo.rank = a.lora.rank;
+  }
   const int grid =
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN));
   TraceScope trace_scope(K_DOWN_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start,
-                     a.tile_desc, a.E, a.H, a.F, dg, du);
+                     a.tile_desc, a.E, a.H, a.F, dg, du, lo);
 }
 
 template <class C>
-void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp, hipStream_t s) {
-  auto k = k_gateup_dgrad<C>;
+void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp, const bf16_t* q1,
+                  hipStream_t s) {
+  const bool lora = q1 != nullptr;
+  auto k = lora ? k_gateup_dgrad<C, true> : k_gateup_dgrad<C, false>;
+  LoraSeg lo;
+  if (lora) {
+    lo.a = q1;
+    lo.b0 = a.lora.a1;
+    lo.rank = a.lora.rank;
+  }
   const int grid =
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
   TraceScope trace_scope(K_GATEUP_DGRAD, s);
   hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start,
-                     a.tile_desc, a.E, a.H, a.F, dxp);
+                     a.tile_desc, a.E, a.H, a.F, dxp, lo);
 }
 
 template <class C, bool F32>
@@ -441,13 +601,22 @@ void gateup_wgrad_any(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, v
 
 hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute) {
   using C = GateUpFwd;
-  auto k = a.xp_rows != nullptr ? k_gateup_fwd<true> : k_gateup_fwd<false>;
+  const bool lora = a.lora.rank > 0;
+  auto k = a.xp_rows != nullptr ? k_gateup_fwd<true, false>
+                                : (lora ? k_gateup_fwd<false, true> : k_gateup_fwd<false, false>);
+  LoraSeg lo;
+  if (lora) {
+    lo.a = a.lora.p1;
+    lo.b0 = a.lora.b1_gate;
+    lo.b1 = a.lora.b1_up;
+    lo.rank = a.lora.rank;
+  }
   const int grid =
       persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
   {
     TraceScope trace_scope(recompute ? K_GATEUP_RECOMPUTE : K_GATEUP_FWD, s);
     hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.xp_rows, a.xp_bytes, a.w_gate, a.w_up,
-                       a.offsets, a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g, a.u, a.act);
+                       a.offsets, a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g, a.u, a.act, lo);
   }
   return hipGetLastError();
 }
@@ -458,15 +627,28 @@ hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t launch_down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, const bf16_t* q2,
+                             hipStream_t s) {
+  if (a.F % 256 == 0) down_dgrad<Wide>(a, d_o, dg, du, q2, s);
+  else down_dgrad<Narrow>(a, d_o, dg, du, q2, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp,
+                               const bf16_t* q1, hipStream_t s) {
+  if (a.H % 256 == 0) gateup_dgrad<Wide>(a, dg, du, dxp, q1, s);
+  else gateup_dgrad<Narrow>(a, dg, du, dxp, q1, s);
+  return hipGetLastError();
+}
+
 hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
                                    bf16_t* dxp, void* dw_down, bool dw_f32, hipStream_t s) {
-  const bool f256 = a.F % 256 == 0, h256 = a.H % 256 == 0;
-  if (f256) down_dgrad<Wide>(a, d_o, dg, du, s);
-  else down_dgrad<Narrow>(a, d_o, dg, du, s);
-  if (h256) down_wgrad_any<Wide>(a, d_o, dw_down, dw_f32, s);
+  if (a.F % 256 == 0) down_dgrad<Wide>(a, d_o, dg, du, nullptr, s);
+  else down_dgrad<Narrow>(a, d_o, dg, du, nullptr, s);
+  if (a.H % 256 == 0) down_wgrad_any<Wide>(a, d_o, dw_down, dw_f32, s);
   else down_wgrad_any<Narrow>(a, d_o, dw_down, dw_f32, s);
-  if (h256) gateup_dgrad<Wide>(a, dg, du, dxp, s);
-  else gateup_dgrad<Narrow>(a, dg, du, dxp, s);
+  if (a.H % 256 == 0) gateup_dgrad<Wide>(a, dg, du, dxp, nullptr, s);
+  else gateup_dgrad<Narrow>(a, dg, du, dxp, nullptr, s);
   return hipGetLastError();
 }
 
@@ -482,6 +664,41 @@ hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg
   const hipError_t e = launch_experts_bwd_data(a, d_o, dg, du, dxp, dw_down, dw_f32, s);
   if (e != hipSuccess) return e;
   return launch_experts_bwd_gateup_w(a, dg, du, dw_gate, dw_up, dw_f32, s);
+}
+
+hipError_t launch_lora_rows(const ExpertArgs& a, const bf16_t* x0, const bf16_t* x1, int64_t ldx,
+                            const bf16_t* w0, const bf16_t* w1, int64_t estride, int K, bool b_kc, bf16_t* out,
+                            hipStream_t s) {
+  using C = LoraRows;
+  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.lora.rank / C::BN);
+  TraceScope trace_scope(K_LORA_ROWS, s);
+#define MOE_LORA_ROWS(KC, NS)                                                                                   \
+  do {                                                                                                          \
+    auto k = k_lora_rows<KC, NS>;                                                                               \
+    hipLaunchKernelGGL(k, dim3(persistent_grid(k, C::kThreads, tiles)), dim3(C::kThreads), 0, s, x0, x1, ldx, w0, \
+                       w1, estride, K, a.tile_start, a.tile_desc, a.E, a.lora.rank, a.lora.scale, out);         \
+  } while (0)
+  if (b_kc) {
+    if (x1 != nullptr) MOE_LORA_ROWS(true, 2);
+    else MOE_LORA_ROWS(true, 1);
+  } else {
+    MOE_LORA_ROWS(false, 1);
+  }
+#undef MOE_LORA_ROWS
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_wgrad(const ExpertArgs& a, const bf16_t* x, int64_t ldx, int M, const bf16_t* y, bool trans,
+                             void* out, bool f32, hipStream_t s) {
+  const int64_t jobs = static_cast<int64_t>(a.E) * (M / LoraW::BM) * (a.lora.rank / LoraW::BN);
+  if (f32) {
+    LoraWgradJobs<true> p{a.offsets, x, ldx, M, y, a.E, a.lora.rank, trans, out};
+    run_stream<false, false>(p, jobs, K_LORA_WGRAD, s);
+  } else {
+    LoraWgradJobs<false> p{a.offsets, x, ldx, M, y, a.E, a.lora.rank, trans, out};
+    run_stream<false, false>(p, jobs, K_LORA_WGRAD, s);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace moe

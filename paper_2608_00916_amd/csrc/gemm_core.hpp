@@ -58,11 +58,16 @@ __device__ __forceinline__ int kc_off(int r, int c) { return r * 128 + ((c ^ ((r
 
 // MN-contiguous tile [64][ROWS]: byte offset of 16-byte unit u of k-row k.
 // The XOR moves 32-byte blocks so that the 16 rows one transposing read
-// touches (k = 8 g + j, g, j < 4) land in distinct banks.
+// touches (k = 8 g + j, g, j < 4) land in distinct banks.  It stays inside
+// the k-row: narrow tiles (16 columns: two units per k-row) keep only the
+// bits of the XOR below their unit count (none for 16 columns, whose 4
+// consecutive k-rows of a read already span distinct banks).
 template <int ROWS>
 __device__ __forceinline__ int mn_off(int k, int u) {
+  static_assert(ROWS >= 16 && (ROWS & (ROWS - 1)) == 0, "MN tiles are a power-of-two number of columns >= 16");
+  constexpr int kUnitMask = ROWS / 8 - 1;
   const int h = (k & 3) | (((k >> 3) & 1) << 2);
-  return k * (ROWS * 2) + ((u ^ (h << 1)) << 4);
+  return k * (ROWS * 2) + ((u ^ ((h << 1) & kUnitMask)) << 4);
 }
 
 // ---------------------------------------------------------------- global -> registers -> LDS
@@ -490,8 +495,8 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   constexpr int kMfma = C::FM * C::FN;
   constexpr int kWrites = LA::kPer + C::NB * LB::kPer;
   constexpr int kLoads = kWrites;
-  static_assert(kReads <= kMfma, "slice reads must fit between the MFMAs of a slice");
-  static_assert(kWrites + kLoads <= kMfma, "refill must fit between the MFMAs of a slice");
+  // the interleave spreads reads, writes and loads evenly over the MFMAs,
+  // also when a small tile has more of them than MFMAs
   auto step = [&](auto set) {
     constexpr int S = decltype(set)::value;
     using Other = std::integral_constant<int, 1 - S>;

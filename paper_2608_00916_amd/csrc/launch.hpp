@@ -9,6 +9,22 @@
 
 namespace moe {
 
+// Rank-r adapters on every expert's gate/up and down projections (rank 0:
+// none): a1 [E,H,r], b1_gate / b1_up [E,r,F], a2 [E,F,r], b2 [E,r,H], and the
+// scale-multiplied rank-r intermediates P1 = scale Xp a1, P2 = scale A a2
+// ([rows_cap][r], written by the forward, read by the backward).
+struct LoraArgs {
+  int rank = 0;
+  float scale = 0.0f;
+  const bf16_t* a1 = nullptr;
+  const bf16_t* b1_gate = nullptr;
+  const bf16_t* b1_up = nullptr;
+  const bf16_t* a2 = nullptr;
+  const bf16_t* b2 = nullptr;
+  bf16_t* p1 = nullptr;
+  bf16_t* p2 = nullptr;
+};
+
 // Operands of the grouped expert products.  Rows are grouped expert-major;
 // offsets[E+1] and tile_start[E+1] (prefix sums of rows and of 128-row tiles
 // per expert) and tile_desc[tile_start[E]] (per 128-row tile: first row,
@@ -29,6 +45,7 @@ struct ExpertArgs {
   // of xp (then the unpermuted tokens, xp_bytes < 2^31 bytes in all).
   const int32_t* xp_rows = nullptr;
   int64_t xp_bytes = 0;
+  LoraArgs lora;
 };
 
 int max_row_tiles(int rows_cap, int E);
@@ -43,6 +60,21 @@ hipError_t launch_down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s);
 hipError_t launch_experts_bwd(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
                               bf16_t* dxp, void* dw_gate, void* dw_up, void* dw_down, bool dw_f32,
                               hipStream_t s);
+// dG, dU (dA += Q2 a2^T with adapters: q2 non-null) and dXp (+= Q1 a1^T: q1).
+hipError_t launch_down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, const bf16_t* q2,
+                             hipStream_t s);
+hipError_t launch_gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp,
+                               const bf16_t* q1, hipStream_t s);
+// Rank-r intermediates: out[r][q] = scale sum_s X_s[r] W_s[e](:, q), X_s
+// [rows][K] (ld ldx), W_s per expert (estride apart) [K][rank] or, b_kc,
+// [rank][K]; x1/w1 a second segment or null.
+hipError_t launch_lora_rows(const ExpertArgs& a, const bf16_t* x0, const bf16_t* x1, int64_t ldx,
+                            const bf16_t* w0, const bf16_t* w1, int64_t estride, int K, bool b_kc, bf16_t* out,
+                            hipStream_t s);
+// Adapter gradients out[e] = X_e^T Y_e (X [rows][M], Y [rows][rank]) stored
+// [E][M][rank] or, trans, [E][rank][M]; bf16 or fp32.
+hipError_t launch_lora_wgrad(const ExpertArgs& a, const bf16_t* x, int64_t ldx, int M, const bf16_t* y, bool trans,
+                             void* out, bool f32, hipStream_t s);
 // The same in two parts, so that work can be queued between them: dG, dU,
 // dW_down and dXp (dxp may alias d_o: it is written last) ...
 hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,

@@ -270,6 +270,122 @@ int recompute_gu(uint32_t flags, ExpertArgs& a, bf16_t* dg, bf16_t* du, hipStrea
   return MOE_OK;
 }
 
+// ---- expert LoRA: argument checks, the saved buffer (the block's layout,
+// then P1 and P2) and the workspace (the larger of the forward's and the
+// backward's, the latter followed by Q1 and Q2)
+int check_lora(const moe_lora* l) {
+  if (l == nullptr) return fail(MOE_ERR_ARG, "lora is NULL");
+  if (l->rank < 16 || l->rank > 64 || l->rank % 16 != 0)
+    return fail(MOE_ERR_SHAPE, "LoRA rank %d must be 16, 32, 48 or 64", l->rank);
+  if (!std::isfinite(l->scale)) return fail(MOE_ERR_ARG, "LoRA scale is not finite");
+  return check_ptrs({{"lora.a1", l->a1}, {"lora.b1_gate", l->b1_gate}, {"lora.b1_up", l->b1_up}, {"lora.a2", l->a2},
+                     {"lora.b2", l->b2}});
+}
+
+bool lora_rank_ok(int32_t rank) { return rank >= 16 && rank <= 64 && rank % 16 == 0; }
+
+struct LoraSaved {
+  bf16_t *p1, *p2;
+  size_t bytes;
+};
+
+LoraSaved lora_saved_layout(const moe_dims* d, int32_t rank, void* base) {
+  const size_t R = static_cast<size_t>(d->T) * d->top_k;
+  Carve c(base);
+  c.off = saved_layout(d, nullptr).bytes;
+  LoraSaved s;
+  s.p1 = c.take<bf16_t>(R * rank);
+  s.p2 = c.take<bf16_t>(R * rank);
+  s.bytes = c.off;
+  return s;
+}
+
+struct LoraWs {
+  bf16_t *q1, *q2;
+  size_t bytes;
+};
+
+LoraWs lora_ws_layout(const moe_dims* d, int32_t rank, void* base) {
+  const size_t R = static_cast<size_t>(d->T) * d->top_k;
+  Carve c(base);
+  c.off = bwd_layout(d, nullptr).bytes;
+  LoraWs w;
+  w.q1 = c.take<bf16_t>(R * rank);
+  w.q2 = c.take<bf16_t>(R * rank);
+  w.bytes = c.off > fwd_ws(d) ? c.off : fwd_ws(d);
+  return w;
+}
+
+LoraArgs lora_args(const moe_lora* l, const LoraSaved& ls) {
+  LoraArgs a;
+  a.rank = l->rank;
+  a.scale = l->scale;
+  a.a1 = static_cast<const bf16_t*>(l->a1);
+  a.b1_gate = static_cast<const bf16_t*>(l->b1_gate);
+  a.b1_up = static_cast<const bf16_t*>(l->b1_up);
+  a.a2 = static_cast<const bf16_t*>(l->a2);
+  a.b2 = static_cast<const bf16_t*>(l->b2);
+  a.p1 = ls.p1;
+  a.p2 = ls.p2;
+  return a;
+}
+
+// The block forward, with the adapters when `lora` is non-null: routing,
+// permutation, router losses, the expert products and the combine.
+int block_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+              const void* w_down, const moe_lora* lora, const uint8_t* token_mask, void* y, void* saved,
+              void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"y", y}, {"saved", saved}, {"ws", ws}}))
+    return rc;
+  if (lora != nullptr)
+    if (int rc = check_lora(lora)) return rc;
+  const bool masked = d->flags & MOE_F_MASK;
+  if (masked && token_mask == nullptr) return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
+  const FwdWs fw = fwd_layout(d, ws);
+  const size_t need = lora != nullptr ? lora_ws_layout(d, lora->rank, nullptr).bytes : fw.bytes;
+  if (ws_bytes < need) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Saved sv = saved_layout(d, saved);
+  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
+  const bf16_t* xb = static_cast<const bf16_t*>(x);
+  hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
+                                   E, k, sv.logits, sv.topk_idx, sv.gates, fw.loss, s);
+  if (e != hipSuccess) return hip_status(e, "router");
+  e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
+                     sv.row_of, sv.xp, fw.perm, s);
+  if (e != hipSuccess) return hip_status(e, "permute");
+  if (fw.loss != nullptr) {
+    e = launch_router_loss(fw.loss, T, E, k, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef,
+                           sv.router_loss, s);
+    if (e != hipSuccess) return hip_status(e, "router losses");
+  }
+  ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
+  if (lora != nullptr) {
+    a.lora = lora_args(lora, lora_saved_layout(d, lora->rank, saved));
+    const int r = lora->rank;
+    // P1 = scale Xp a1 (a1 [E][H][r]: the B operand MN-contiguous)
+    e = launch_lora_rows(a, sv.xp, nullptr, H, a.lora.a1, nullptr, static_cast<int64_t>(H) * r, H, false,
+                         a.lora.p1, s);
+    if (e != hipSuccess) return hip_status(e, "LoRA P1");
+  }
+  e = launch_gateup_fwd(a, s);
+  if (e != hipSuccess) return hip_status(e, "gate/up");
+  if (lora != nullptr) {
+    const int r = lora->rank;
+    // P2 = scale A a2 (a2 [E][F][r])
+    e = launch_lora_rows(a, sv.a, nullptr, F, a.lora.a2, nullptr, static_cast<int64_t>(F) * r, F, false, a.lora.p2,
+                         s);
+    if (e != hipSuccess) return hip_status(e, "LoRA P2");
+  }
+  e = launch_down_fwd(a, sv.o, s);
+  if (e != hipSuccess) return hip_status(e, "down");
+  e = launch_combine(sv.o, sv.gates, sv.row_of, T, H, k, static_cast<bf16_t*>(y), s);
+  return hip_status(e, "combine");
+}
+
 }  // namespace
 
 extern "C" {
@@ -312,37 +428,7 @@ int moe_saved_views(const moe_dims* d, void* saved, moe_saved_view* v) {
 int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
             const void* w_down, const uint8_t* token_mask, void* y, void* saved, void* ws,
             size_t ws_bytes, void* stream) {
-  if (int rc = check_dims(d)) return rc;
-  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
-                           {"y", y}, {"saved", saved}, {"ws", ws}}))
-    return rc;
-  const bool masked = d->flags & MOE_F_MASK;
-  if (masked && token_mask == nullptr) return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
-  const FwdWs fw = fwd_layout(d, ws);
-  if (ws_bytes < fw.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, fw.bytes);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Saved sv = saved_layout(d, saved);
-  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
-  const bf16_t* xb = static_cast<const bf16_t*>(x);
-  hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, sv.logits, sv.topk_idx, sv.gates, fw.loss, s);
-  if (e != hipSuccess) return hip_status(e, "router");
-  e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
-                     sv.row_of, sv.xp, fw.perm, s);
-  if (e != hipSuccess) return hip_status(e, "permute");
-  if (fw.loss != nullptr) {
-    e = launch_router_loss(fw.loss, T, E, k, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef,
-                           sv.router_loss, s);
-    if (e != hipSuccess) return hip_status(e, "router losses");
-  }
-  ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
-               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
-  e = launch_gateup_fwd(a, s);
-  if (e != hipSuccess) return hip_status(e, "gate/up");
-  e = launch_down_fwd(a, sv.o, s);
-  if (e != hipSuccess) return hip_status(e, "down");
-  e = launch_combine(sv.o, sv.gates, sv.row_of, T, H, k, static_cast<bf16_t*>(y), s);
-  return hip_status(e, "combine");
+  return block_fwd(d, x, w_r, w_gate, w_up, w_down, nullptr, token_mask, y, saved, ws, ws_bytes, stream);
 }
 
 int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
@@ -377,6 +463,76 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   if (e != hipSuccess) return hip_status(e, "experts bwd");
   e = launch_dwr(static_cast<const bf16_t*>(x), w.dz, T, H, E, w.dwr_part, dw_r, f32, s);
   return hip_status(e, "router weight grad");
+}
+
+size_t moe_lora_saved_bytes(const moe_dims* d, int32_t rank) {
+  if (check_dims(d) != MOE_OK || !lora_rank_ok(rank)) return 0;
+  return lora_saved_layout(d, rank, nullptr).bytes;
+}
+
+size_t moe_lora_workspace_bytes(const moe_dims* d, int32_t rank) {
+  if (check_dims(d) != MOE_OK || !lora_rank_ok(rank)) return 0;
+  return lora_ws_layout(d, rank, nullptr).bytes;
+}
+
+int moe_lora_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+                 const void* w_down, const moe_lora* lora, const uint8_t* token_mask, void* y, void* saved,
+                 void* ws, size_t ws_bytes, void* stream) {
+  if (lora == nullptr) return fail(MOE_ERR_ARG, "lora is NULL");
+  return block_fwd(d, x, w_r, w_gate, w_up, w_down, lora, token_mask, y, saved, ws, ws_bytes, stream);
+}
+
+int moe_lora_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+                 const void* w_down, const moe_lora* lora, const void* dy, const void* saved, void* dx, void* da1,
+                 void* db1_gate, void* db1_up, void* da2, void* db2, void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"dy", dy}, {"saved", saved}, {"dx", dx}, {"da1", da1}, {"db1_gate", db1_gate},
+                           {"db1_up", db1_up}, {"da2", da2}, {"db2", db2}, {"ws", ws}}))
+    return rc;
+  if (int rc = check_lora(lora)) return rc;
+  const LoraWs lw = lora_ws_layout(d, lora->rank, ws);
+  if (ws_bytes < lw.bytes) return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, lw.bytes);
+  const BwdWs w = bwd_layout(d, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Saved sv = saved_layout(d, const_cast<void*>(saved));
+  const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k, r = lora->rank;
+  const bool f32 = d->flags & MOE_F_DW_FP32;
+  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
+                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, sv.logits, sv.counts,
+                                    sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+  if (e != hipSuccess) return hip_status(e, "combine bwd");
+  ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
+               static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
+  a.lora = lora_args(lora, lora_saved_layout(d, r, const_cast<void*>(saved)));
+  if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
+  // Q2 = scale dO b2^T (b2 [E][r][H]: rows q of the B operand, K-contiguous)
+  e = launch_lora_rows(a, w.d_o, nullptr, H, a.lora.b2, nullptr, static_cast<int64_t>(r) * H, H, true, lw.q2, s);
+  if (e != hipSuccess) return hip_status(e, "LoRA Q2");
+  e = launch_down_dgrad(a, w.d_o, w.dg, w.du, lw.q2, s);
+  if (e != hipSuccess) return hip_status(e, "down dgrad");
+  // d a2 = A^T Q2 ([E][F][r]); d b2 = P2^T dO, formed as (dO^T P2)^T ([E][r][H])
+  e = launch_lora_wgrad(a, sv.a, F, F, lw.q2, false, da2, f32, s);
+  if (e != hipSuccess) return hip_status(e, "LoRA d a2");
+  e = launch_lora_wgrad(a, w.d_o, H, H, a.lora.p2, true, db2, f32, s);
+  if (e != hipSuccess) return hip_status(e, "LoRA d b2");
+  // Q1 = scale (dG b1_gate^T + dU b1_up^T)
+  e = launch_lora_rows(a, w.dg, w.du, F, a.lora.b1_gate, a.lora.b1_up, static_cast<int64_t>(r) * F, F, true, lw.q1,
+                       s);
+  if (e != hipSuccess) return hip_status(e, "LoRA Q1");
+  // dXp (+ Q1 a1^T) into dO's memory: everything that reads dO is queued above
+  e = launch_gateup_dgrad(a, w.dg, w.du, w.d_o, lw.q1, s);
+  if (e != hipSuccess) return hip_status(e, "gate/up dgrad");
+  e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
+                       w.w_rt, static_cast<bf16_t*>(dx), w.dense != nullptr ? w.dz : nullptr, w.dense, s);
+  if (e != hipSuccess) return hip_status(e, "dx");
+  // d a1 = Xp^T Q1 ([E][H][r]); d b1 = P1^T dG / dU, formed transposed ([E][r][F])
+  e = launch_lora_wgrad(a, sv.xp, H, H, lw.q1, false, da1, f32, s);
+  if (e != hipSuccess) return hip_status(e, "LoRA d a1");
+  e = launch_lora_wgrad(a, w.dg, F, F, a.lora.p1, true, db1_gate, f32, s);
+  if (e != hipSuccess) return hip_status(e, "LoRA d b1_gate");
+  e = launch_lora_wgrad(a, w.du, F, F, a.lora.p1, true, db1_up, f32, s);
+  return hip_status(e, "LoRA d b1_up");
 }
 
 size_t moe_infer_workspace_bytes(const moe_dims* d) {

@@ -31,6 +31,8 @@ enum KernelId {
   K_GATEUP_RECOMPUTE,
   K_ROUTER_LOSS,
   K_ROUTER_DX_DENSE,
+  K_LORA_ROWS,
+  K_LORA_WGRAD,
   K_NUM_KERNELS
 };
 

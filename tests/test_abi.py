@@ -171,3 +171,28 @@ def test_router_loss_workspaces():
     v = _lib.MoeSavedView()
     assert L.moe_saved_views(ctypes.byref(da), 1 << 20, ctypes.byref(v)) == 0
     assert v.router_loss is not None and v.router_loss % 256 == 0
+
+
+def test_lora_sizes_and_errors():
+    L = _lib.lib()
+    d = D()
+    base = L.moe_saved_bytes(ctypes.byref(d))
+    assert L.moe_lora_saved_bytes(ctypes.byref(d), 16) >= base + 2 * 256 * 2 * 16 * 2
+    assert L.moe_lora_workspace_bytes(ctypes.byref(d), 32) >= L.moe_bwd_workspace_bytes(ctypes.byref(d))
+    for bad in (0, 8, 24, 80):
+        assert L.moe_lora_saved_bytes(ctypes.byref(d), bad) == 0
+    lo = _lib.MoeLora(16, 2.0, FAKE, FAKE, FAKE, FAKE, FAKE)
+    ws = 1 << 40
+
+    def fwd_l(lora, dims=d):
+        return L.moe_lora_fwd(ctypes.byref(dims), FAKE, FAKE, FAKE, FAKE, FAKE, lora, None, FAKE, FAKE, FAKE, ws,
+                              None)
+    assert fwd_l(None) == _lib.MOE_ERR_ARG
+    assert fwd_l(ctypes.byref(_lib.MoeLora(24, 2.0, FAKE, FAKE, FAKE, FAKE, FAKE))) == _lib.MOE_ERR_SHAPE
+    assert fwd_l(ctypes.byref(_lib.MoeLora(16, float("nan"), FAKE, FAKE, FAKE, FAKE, FAKE))) == _lib.MOE_ERR_ARG
+    assert fwd_l(ctypes.byref(_lib.MoeLora(16, 2.0, FAKE, None, FAKE, FAKE, FAKE))) == _lib.MOE_ERR_ARG
+    assert fwd_l(ctypes.byref(_lib.MoeLora(16, 2.0, FAKE, FAKE, FAKE, FAKE + 2, FAKE))) == _lib.MOE_ERR_ALIGN
+    assert L.moe_lora_bwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(lo), FAKE, FAKE, FAKE, FAKE,
+                          FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == _lib.MOE_ERR_WORKSPACE
+    assert L.moe_lora_bwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(lo), FAKE, FAKE, FAKE, None,
+                          FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == _lib.MOE_ERR_ARG
