@@ -175,6 +175,39 @@ def serving_forward(moe, t, tm, T, H, E, F, k, Tv, steps, warmup):
             "tflops": 6.0 * H * F * Tv * k / (ms * 1e-3) / 1e12}
 
 
+def lora_step(moe, t, tm, T, H, E, F, k, Tv, rank, steps, warmup):
+    """Forward + backward with rank-r expert adapters (base weights and router
+    frozen) on the same batch, timed after the other regions."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+
+    def w(*shape):
+        return (0.02 * torch.randn(shape, generator=g, device="cuda")).to(torch.bfloat16)
+    ad = dict(a1=w(E, H, rank), b1_gate=w(E, rank, F), b1_up=w(E, rank, F), a2=w(E, F, rank), b2=w(E, rank, H))
+    lora = moe.lora_args(rank, 2.0, ad["a1"], ad["b1_gate"], ad["b1_up"], ad["a2"], ad["b2"])
+    blk = moe.MoELoRA(T, H, E, F, k, rank, mask=tm is not None)
+
+    def run():
+        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], lora, tm)
+        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], lora, t["dy"])
+
+    for _ in range(warmup):
+        run()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(f"[bench] expert LoRA (rank {rank}) fwd+bwd: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    return {"entry": "moe_lora_fwd + moe_lora_bwd", "rank": rank, "tokens_per_s": Tv / (ms * 1e-3),
+            "ms_per_step": ms, "steps": steps}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -187,7 +220,8 @@ def main():
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the kernel region (per-kernel events, roofline)")
     ap.add_argument("--no-forward-only", action="store_true",
-                    help="skip the forward-only (moe_infer) timing")
+                    help="skip the forward-only (moe_infer) and expert-LoRA timings")
+    ap.add_argument("--lora-rank", type=int, default=16, help="rank of the expert-LoRA timing")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one torch copy of MIB MiB before the steps (counter calibration)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -291,6 +325,8 @@ def main():
               "step_ms": pct([m[0].elapsed_time(m[2]) for m in marks])}
     forward_only = None if args.no_forward_only else serving_forward(moe, t, tm, T, H, E, F, k, Tv, args.steps,
                                                                      args.warmup)
+    lora = None if args.no_forward_only else lora_step(moe, t, tm, T, H, E, F, k, Tv, args.lora_rank,
+                                                       args.steps, args.warmup)
 
     gemm_flop = 18.0 * H * F * R
     router_flop = 6.0 * H * E * Tv
@@ -314,6 +350,7 @@ def main():
         "block_frac_bf16_peak": tflops / PEAK_BF16_TFLOPS,
         "timing": timing,
         "forward_only": forward_only,
+        "expert_lora": lora,
     }
     if traced_ms is not None:
         out["kernel_region_ms_per_step"] = traced_ms
