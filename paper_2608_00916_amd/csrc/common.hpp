@@ -17,6 +17,16 @@ __device__ __forceinline__ float bf2f(bf16_t v) {
   return __uint_as_float(static_cast<uint32_t>(v) << 16);
 }
 
+// A value every lane reads from the same address, loaded through the scalar
+// data cache (constant address space).  Its wait then counts scalar loads
+// only: a vector load of it would be followed by a wait for every vector
+// load and store in flight.  Only for data that no running kernel writes
+// (the scalar cache is invalidated at each kernel start, not during it).
+template <class T>
+__device__ __forceinline__ T uniform_load(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)(p);
+}
+
 // Round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16_t f2bf(float v) {
   __bf16 b = static_cast<__bf16>(v);

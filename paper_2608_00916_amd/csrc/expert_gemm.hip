@@ -333,19 +333,26 @@ struct DownWgradJobs {
   __device__ bool get(int i, Job<C>& j) const {
     int e, m0, n0;
     if (!wgrad_locate<C>(i, E, F, H, e, m0, n0)) return false;
-    const int r0 = offsets[e];
+    const int r0 = uniform_load(offsets + e);
     j.a = act + static_cast<int64_t>(r0) * F + m0;
     j.lda = F;
     j.m_lim = C::BM;
     j.b[0] = d_o + static_cast<int64_t>(r0) * H + n0;
     j.ldb = H;
     j.n_lim = C::BN;
-    j.K = offsets[e + 1] - r0;
+    j.K = uniform_load(offsets + e + 1) - r0;
     j.chain = false;
     j.e = e;
     j.m0 = m0;
     j.n0 = n0;
     return true;
+  }
+  // bf16 gradients leave through the LDS staging area
+  static constexpr bool kStaged = !F32;
+  __device__ void stage_dst(const Job<C>& j, bf16_t* (&dst)[C::NB], int64_t& ld, int& rows) const {
+    dst[0] = static_cast<bf16_t*>(dw_down) + static_cast<int64_t>(j.e) * F * H + static_cast<int64_t>(j.m0) * H + j.n0;
+    ld = H;
+    rows = C::BM;
   }
   __device__ void epilogue(const Job<C>& j, f32x4 (&acc)[C::FM][C::FN]) const {
     const int lane = threadIdx.x & 63;
@@ -370,7 +377,7 @@ struct GateUpWgradJobs {
   __device__ bool get(int i, Job<C>& j) const {
     int e, m0, n0;
     if (!wgrad_locate<C>(i, E, H, F, e, m0, n0)) return false;
-    const int r0 = offsets[e];
+    const int r0 = uniform_load(offsets + e);
     const int64_t bofs = static_cast<int64_t>(r0) * F + n0;
     j.a = xp + static_cast<int64_t>(r0) * H + m0;
     j.lda = H;
@@ -379,12 +386,20 @@ struct GateUpWgradJobs {
     j.b[1] = du_in + bofs;
     j.ldb = F;
     j.n_lim = C::BNS;
-    j.K = offsets[e + 1] - r0;
+    j.K = uniform_load(offsets + e + 1) - r0;
     j.chain = false;
     j.e = e;
     j.m0 = m0;
     j.n0 = n0;
     return true;
+  }
+  static constexpr bool kStaged = !F32;
+  __device__ void stage_dst(const Job<C>& j, bf16_t* (&dst)[C::NB], int64_t& ld, int& rows) const {
+    const int64_t o = static_cast<int64_t>(j.e) * H * F + static_cast<int64_t>(j.m0) * F + j.n0;
+    dst[0] = static_cast<bf16_t*>(dw_gate) + o;
+    dst[1] = static_cast<bf16_t*>(dw_up) + o;
+    ld = F;
+    rows = C::BM;
   }
   __device__ void epilogue(const Job<C>& j, f32x4 (&acc)[C::FM][C::FN]) const {
     const int lane = threadIdx.x & 63;
@@ -423,7 +438,7 @@ struct LoraWgradJobs {
     if (logical >= E * nm * nq) return false;
     const int e = logical / (nm * nq);
     const int rem = logical - e * nm * nq;
-    const int r0 = offsets[e];
+    const int r0 = uniform_load(offsets + e);
     j.m0 = (rem / nq) * C::BM;
     j.n0 = (rem % nq) * C::BN;
     j.a = x + static_cast<int64_t>(r0) * ldx + j.m0;
@@ -432,7 +447,7 @@ struct LoraWgradJobs {
     j.b[0] = y + static_cast<int64_t>(r0) * rank + j.n0;
     j.ldb = rank;
     j.n_lim = C::BN;
-    j.K = offsets[e + 1] - r0;
+    j.K = uniform_load(offsets + e + 1) - r0;
     j.chain = false;
     j.e = e;
     return true;
@@ -461,7 +476,7 @@ struct LoraWgradJobs {
 // One persistent kernel for every product: the job provider decides.
 template <class P, bool A_KC, bool B_KC>
 __global__ __launch_bounds__(P::C::kThreads) void k_stream(P prov) {
-  __shared__ __attribute__((aligned(16))) char smem[P::C::kLds];
+  __shared__ __attribute__((aligned(16))) char smem[stream_lds<P>()];
   gemm_stream<typename P::C, A_KC, B_KC>(prov, smem);
 }
 

@@ -36,6 +36,7 @@ namespace moe {
 constexpr int BK = 64;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
 #define MOE_LDS __attribute__((address_space(3)))
 
 // BM x BN tile computed by WM x WN waves (each (BM/WM) x (BN/WN)).
@@ -391,6 +392,67 @@ __device__ __forceinline__ void gemm_mainloop(const bf16_t* a, int64_t lda, int 
 // A workgroup's sequence of tile jobs.  A job is one tile's K range of one
 // product; `chain` jobs accumulate into the next job's tile (a K range split
 // over two operand pairs) instead of ending it.
+// Output coordinates of fragment (mi, ni) for this lane: row, first of 4 columns
+// (columns index the B tile: [0, BN/2) first operand, [BN/2, BN) second when NB = 2).
+template <class C>
+__device__ __forceinline__ int frag_row(int mi, int lane) {
+  const int wm = (threadIdx.x >> 6) / C::WN;
+  return wm * (C::BM / C::WM) + mi * 16 + (lane & 15);
+}
+template <class C>
+__device__ __forceinline__ int frag_col(int ni, int lane) {
+  const int wn = (threadIdx.x >> 6) % C::WN;
+  return brow<C>(wn, ni) + 4 * (lane >> 4);
+}
+
+__device__ __forceinline__ uint2 pack4_bf16(const f32x4& v) {
+  return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+}
+
+// ---------------------------------------------------------------- staged output
+// A job provider that declares `static constexpr bool kStaged = true` hands
+// its finished tiles over as bf16 through LDS instead of storing them from
+// the accumulators: after a tile's last K step the workgroup writes the tile
+// into an LDS staging area, and each following K step stores one slice of it
+// (one 16-byte chunk per thread) to global memory.  The stores then overlap
+// the next tile's MFMAs; stored straight from the accumulators they stall
+// every wave at the tile boundary until they complete (one counter tracks
+// both loads and stores), which costs as much as the tile's MFMAs when the
+// reduction is short (weight gradients over one expert's rows).
+// P::stage_dst(job, dst, ld, rows) names the NB destinations (element (0, 0)
+// of each BM x BNS block, row pitch ld elements, `rows` valid rows); whole
+// rows of BNS columns are written.
+template <class C>
+struct Staged {
+  static constexpr int kRowBytes = C::BN * 2;                   // one tile row, all NB blocks
+  static constexpr int kBytes = C::BM * kRowBytes;              // LDS staging area
+  static constexpr int kCpr = C::BNS * 2 / 16;                  // 16-byte chunks per block row
+  static constexpr int kRowsPerWave = 64 / kCpr;                // block rows one wave stores per slice
+  static constexpr int kWavesPerDst = C::kThreads / 64 / C::NB;
+  static constexpr int kSliceRows = kWavesPerDst * kRowsPerWave;
+  static constexpr int kSlices = C::BM / kSliceRows;
+  static constexpr int kXor = (C::BN / 8 < 16 ? C::BN / 8 : 16) - 1;  // chunk swizzle: rows of 16 hit distinct banks
+  static_assert(64 % kCpr == 0 && (C::kThreads / 64) % C::NB == 0, "a wave stores whole block rows of one block");
+  static_assert(kSlices * kSliceRows == C::BM && kSliceRows % 16 == 0, "slices of 16k rows keep the swizzle fixed");
+  // byte offset of chunk q (0 .. BN/8) of tile row r in the staging area
+  static __device__ __forceinline__ int off(int r, int q) { return r * kRowBytes + ((q ^ (r & kXor)) << 4); }
+};
+
+template <class P, class = void>
+struct staged_provider : std::false_type {};
+template <class P>
+struct staged_provider<P, std::void_t<decltype(P::kStaged)>> : std::integral_constant<bool, P::kStaged> {};
+
+// LDS bytes gemm_stream needs for provider P.
+template <class P>
+constexpr int stream_lds() {
+  return P::C::kLds + (staged_provider<P>::value ? Staged<typename P::C>::kBytes : 0);
+}
+
+__device__ __forceinline__ void buf_store16(__amdgpu_buffer_rsrc_t r, uint32_t off, const uint4& v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), r, static_cast<int>(off), 0, 0);
+}
+
 template <class C>
 struct Job {
   const bf16_t* a;
@@ -412,6 +474,9 @@ struct Job {
 // tile's last steps and its epilogue.
 template <class C, bool A_KC, bool B_KC, class P>
 __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
+  static_assert(std::is_same<C, typename P::C>::value, "the provider's tile shape");
+  constexpr bool kStaged = staged_provider<P>::value;
+  using SO = Staged<C>;
   using LA = Loader<A_KC, C::BM, C::BM, C::kThreads>;
   using LB = Loader<B_KC, C::BNS, C::BN, C::kThreads>;
   using S0 = std::integral_constant<int, 0>;
@@ -465,6 +530,58 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     for (int i = 0; i < C::NB; ++i) lb[i].store(rb[S][i], stage + C::kABytes, i * C::BNS, tid);
   };
 
+  // staged output (kStaged): this thread's chunk of every slice, the current
+  // destination and the next slice to store (kSlices: none pending)
+  char* const stg = smem + C::kLds;
+  int d_lds = 0, d_row = 0, d_col = 0;
+  if constexpr (kStaged) {
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int h = wv % C::NB, cq = lane % SO::kCpr;
+    d_row = (wv / C::NB) * SO::kRowsPerWave + lane / SO::kCpr;
+    d_col = cq * 16;
+    d_lds = SO::off(d_row, h * SO::kCpr + cq);
+  }
+  __amdgpu_buffer_rsrc_t d_rsrc = make_rsrc(nullptr, 0);
+  uint32_t d_ld = 0;
+  int d_slice = SO::kSlices;
+  auto drain_one = [&](int slice) {  // slice < kSlices stores, else nothing (a branch-free no-op)
+    const int sl = slice < SO::kSlices ? slice : SO::kSlices - 1;
+    const uint4 v = *reinterpret_cast<const uint4*>(stg + d_lds + sl * (SO::kSliceRows * SO::kRowBytes));
+    const uint32_t off = static_cast<uint32_t>(d_row + sl * SO::kSliceRows) * d_ld + d_col;
+    buf_store16(d_rsrc, slice < SO::kSlices ? off : kOob, v);
+  };
+  auto finish = [&](const Job<C>& j) {  // a finished tile: epilogue, or into the staging area
+    if constexpr (kStaged) {
+      if (d_slice < SO::kSlices) {  // the previous tile is not fully stored yet (short K)
+        for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
+        lds_barrier();
+      }
+      const int wv = tid >> 6;
+      const int wm_ = wv / C::WN;
+#pragma unroll
+      for (int mi = 0; mi < C::FM; ++mi) {
+        const int r = wm_ * (C::BM / C::WM) + mi * 16 + (lane & 15);
+#pragma unroll
+        for (int ni = 0; ni < C::FN; ++ni) {
+          const int c = frag_col<C>(ni, lane);
+          *reinterpret_cast<uint2*>(stg + SO::off(r, c >> 3) + (c & 7) * 2) = pack4_bf16(acc[mi][ni]);
+        }
+      }
+      bf16_t* dst[C::NB];
+      int64_t ld;
+      int rows;
+      prov.stage_dst(j, dst, ld, rows);
+      const int h = __builtin_amdgcn_readfirstlane(tid >> 6) % C::NB;
+      const int64_t bytes = rows > 0 ? static_cast<int64_t>(rows - 1) * ld * 2 + C::BNS * 2 : 0;
+      d_rsrc = make_rsrc(dst[h], bytes);
+      d_ld = static_cast<uint32_t>(ld * 2);
+      d_slice = 0;
+      lds_barrier();
+    } else {
+      prov.epilogue(j, acc);
+    }
+  };
+
   // compute cursor: job ci, step ckt
   int ci = 0, ckt = 0;
   Job<C> cj;
@@ -472,7 +589,7 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   auto csettle = [&]() {  // finish empty jobs (their tiles are zero unless chained)
     while (cok && cj.K <= 0) {
       if (!cj.chain) {
-        prov.epilogue(cj, acc);
+        finish(cj);
         zero_acc<C>(acc);
       }
       cok = prov.get(++ci, cj);
@@ -483,7 +600,7 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     if (++ckt * BK >= cj.K) {
       ckt = 0;
       if (!cj.chain) {
-        prov.epilogue(cj, acc);
+        finish(cj);
         zero_acc<C>(acc);
       }
       cok = prov.get(++ci, cj);
@@ -503,20 +620,35 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     const char* cur = smem + S * C::kStage;
     char* nxt = smem + (1 - S) * C::kStage;
     uint4 af0[C::FM], bf0[C::FN], af1[C::FM], bf1[C::FN];
+    // staged output: two slices in the first step of each pair; their stores
+    // then have two steps to complete before a wait for later loads needs them
+    constexpr int kDrain = kStaged && S == 0 ? 2 : 0;
+    if constexpr (kDrain > 0) {
+      drain_one(d_slice);
+      drain_one(d_slice + 1);
+    }
     read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 0, lane, af0, bf0);
     read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 1, lane, af1, bf1);
     mfmas<C>(af0, bf0, acc);
     mfmas<C>(af1, bf1, acc);
     store(Other{}, nxt);
     load(Other{});
-    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads + kDrain, 0);
     interleave<kMfma, kReads, 0x100, 0, 0x200>();
     interleave<kMfma, kWrites, 0x200, kLoads, 0x020>();
+    if constexpr (kDrain > 0) {
+      __builtin_amdgcn_sched_group_barrier(0x040, kDrain, 0);  // the staged slices' stores
+      d_slice = d_slice + kDrain < SO::kSlices ? d_slice + kDrain : SO::kSlices;
+    }
     lds_barrier();
     lnext();
   };
 
-  if (!cok) return;
+  if (!cok) {  // only empty jobs: the last of them may still be staged
+    if constexpr (kStaged)
+      for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
+    return;
+  }
   load(S0{});
   lnext();
   load(S1{});
@@ -525,32 +657,19 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   lds_barrier();
   load(S0{});
   lnext();
-  while (cok) {
+  for (;;) {  // cok holds here (checked above); every exit is a break
     step(S0{});
     cadvance();
     if (!cok) break;
     step(S1{});
     cadvance();
+    if (!cok) break;
   }
+  if constexpr (kStaged)
+    for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
   lds_barrier();  // the workgroup's LDS is free again
 }
 
-// Output coordinates of fragment (mi, ni) for this lane: row, first of 4 columns
-// (columns index the B tile: [0, BN/2) first operand, [BN/2, BN) second when NB = 2).
-template <class C>
-__device__ __forceinline__ int frag_row(int mi, int lane) {
-  const int wm = (threadIdx.x >> 6) / C::WN;
-  return wm * (C::BM / C::WM) + mi * 16 + (lane & 15);
-}
-template <class C>
-__device__ __forceinline__ int frag_col(int ni, int lane) {
-  const int wn = (threadIdx.x >> 6) % C::WN;
-  return brow<C>(wn, ni) + 4 * (lane >> 4);
-}
-
-__device__ __forceinline__ uint2 pack4_bf16(const f32x4& v) {
-  return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-}
 
 // Blocks are dispatched round-robin over the 8 XCDs (each with its own L2);
 // give each XCD a contiguous range of logical tiles so that neighbouring
