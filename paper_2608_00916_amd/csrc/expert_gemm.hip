@@ -105,25 +105,20 @@ __global__ __launch_bounds__(LoraRows::kThreads) void k_lora_rows(
   });
 }
 
-// G = Xp W_gate[e], U = Xp W_up[e], A = silu(G) * U  (K = H, N = F).
-// The B tile holds 128 columns of W_gate next to the same 128 of W_up.
-// G and U are stored when g_out is non-null, A when a_out is.  With xp_rows
-// non-null, row r of the product is row xp_rows[r] of xp (the gather read
-// through the permutation; xp_bytes bounds xp).
-// With kLora the adapters' rank-r term joins as one more K segment:
-// [G | U] += P1 [b1_gate | b1_up][e] (P1 = scale Xp a1, [rows][r]).
 using GateUpFwd = Tile<128, 256, 2, 2, 4>;
-template <bool kRows, bool kLora>
-__global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t* __restrict__ xp,
-                                                         const int32_t* __restrict__ xp_rows,
-                                                         int64_t xp_bytes,
-                                                         const bf16_t* __restrict__ w_gate,
-                                                         const bf16_t* __restrict__ w_up,
-                                                         const int32_t* __restrict__ offsets,
-                                                         const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
-                                                         int H, int F, bf16_t* __restrict__ g_out,
-                                                         bf16_t* __restrict__ u_out,
-                                                         bf16_t* __restrict__ a_out, LoraSeg lo) {
+
+// G = X W_gate[e], U = X W_up[e], A = silu(G) * U (K = H, N = F) with row r
+// of the product read from row xp_rows[r] of xp (the tokens themselves,
+// gathered through the permutation; xp_bytes bounds xp): the forward-only
+// pass, which skips the permuted copy.  The B tile holds 128 columns of
+// W_gate next to the same 128 of W_up; the SwiGLU takes the bf16-rounded G
+// and U, as the streamed kernel does.  G and U are stored when g_out is
+// non-null, A when a_out is.
+__global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd_rows(
+    const bf16_t* __restrict__ xp, const int32_t* __restrict__ xp_rows, int64_t xp_bytes,
+    const bf16_t* __restrict__ w_gate, const bf16_t* __restrict__ w_up, const int32_t* __restrict__ tile_start,
+    const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* __restrict__ g_out, bf16_t* __restrict__ u_out,
+    bf16_t* __restrict__ a_out) {
   using C = GateUpFwd;
   static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
@@ -133,17 +128,7 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
     const int n0 = t.nt * C::BNS;
     const int64_t wofs = static_cast<int64_t>(t.e) * H * F + n0;
     const bf16_t* bs[2] = {w_gate + wofs, w_up + wofs};
-    if constexpr (kRows)
-      gemm_mainloop<C, true, false>(xp, H, t.m_lim, bs, F, F - n0, H, smem, acc, xp_rows + t.m0, xp_bytes);
-    else
-      gemm_mainloop<C, true, false>(xp + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, F, F - n0, H, smem,
-                                    acc);
-    if constexpr (kLora) {  // b1 is [E][r][F]: MN-contiguous like W_gate
-      const int64_t lofs = static_cast<int64_t>(t.e) * lo.rank * F + n0;
-      const bf16_t* bl[2] = {lo.b0 + lofs, lo.b1 + lofs};
-      gemm_mainloop<C, true, false>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, F, F - n0,
-                                    lo.rank, smem, acc);
-    }
+    gemm_mainloop<C, true, false>(xp, H, t.m_lim, bs, F, F - n0, H, smem, acc, xp_rows + t.m0, xp_bytes);
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
@@ -153,147 +138,18 @@ __global__ __launch_bounds__(GateUpFwd::kThreads) void k_gateup_fwd(const bf16_t
 #pragma unroll
       for (int ni = 0; ni < C::FN / 2; ++ni) {
         const int c = frag_col<C>(ni, lane);  // column within the W_gate half
-        const f32x4 gv = acc[mi][ni], uv = acc[mi][ni + C::FN / 2];
+        const uint2 gw = pack4_bf16(acc[mi][ni]), uw = pack4_bf16(acc[mi][ni + C::FN / 2]);
+        const float gv[4] = {lo_bf(gw.x), hi_bf(gw.x), lo_bf(gw.y), hi_bf(gw.y)};
+        const float uv[4] = {lo_bf(uw.x), hi_bf(uw.x), lo_bf(uw.y), hi_bf(uw.y)};
         f32x4 av;
 #pragma unroll
         for (int i = 0; i < 4; ++i) av[i] = silu_f(gv[i]) * uv[i];
         if (g_out != nullptr) {
-          *reinterpret_cast<uint2*>(g_out + base + c) = pack4_bf16(gv);
-          *reinterpret_cast<uint2*>(u_out + base + c) = pack4_bf16(uv);
+          *reinterpret_cast<uint2*>(g_out + base + c) = gw;
+          *reinterpret_cast<uint2*>(u_out + base + c) = uw;
         }
         if (a_out != nullptr) *reinterpret_cast<uint2*>(a_out + base + c) = pack4_bf16(av);
       }
-    }
-  });
-}
-
-// O = A W_down[e]  (K = F, N = H); with kLora also O += P2 b2[e]
-// (P2 = scale A a2, [rows][r]; b2 [E][r][H] MN-contiguous).
-template <class C, bool kLora>
-__global__ __launch_bounds__(C::kThreads) void k_down_fwd(const bf16_t* __restrict__ act,
-                                                       const bf16_t* __restrict__ w_down,
-                                                       const int32_t* __restrict__ offsets,
-                                                       const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E,
-                                                       int H, int F, bf16_t* __restrict__ o_out, LoraSeg lo) {
-  static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
-    f32x4 acc[C::FM][C::FN];
-    zero_acc<C>(acc);
-    const int n0 = t.nt * C::BN;
-    const bf16_t* bs[1] = {w_down + static_cast<int64_t>(t.e) * F * H + n0};
-    gemm_mainloop<C, true, false>(act + static_cast<int64_t>(t.m0) * F, F, t.m_lim, bs, H, H - n0, F, smem,
-                                  acc);
-    if constexpr (kLora) {
-      const bf16_t* bl[1] = {lo.b0 + static_cast<int64_t>(t.e) * lo.rank * H + n0};
-      gemm_mainloop<C, true, false>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, H, H - n0,
-                                    lo.rank, smem, acc);
-    }
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int mi = 0; mi < C::FM; ++mi) {
-      const int r = frag_row<C>(mi, lane);
-      if (r >= t.m_lim) continue;
-      const int64_t base = static_cast<int64_t>(t.m0 + r) * H + n0;
-#pragma unroll
-      for (int ni = 0; ni < C::FN; ++ni)
-        *reinterpret_cast<uint2*>(o_out + base + frag_col<C>(ni, lane)) = pack4_bf16(acc[mi][ni]);
-    }
-  });
-}
-
-// dA = dO W_down[e]^T (K = H, N = F) fused with the SwiGLU backward:
-// s = sigmoid(G); dG = dA U s (1 + G (1 - s)); dU = dA G s.
-// dG and dU may overwrite G and U in place: each lane reads an element of G
-// and U before it writes the same element of dG and dU, and nothing else
-// reads them.
-// With kLora dA also takes Q2 a2[e]^T (Q2 = scale dO b2^T, [rows][r]; a2
-// [E][F][r]: K-contiguous rows of the B tile).
-template <class C, bool kLora>
-__global__ __launch_bounds__(C::kThreads) void k_down_dgrad_swiglu(
-    const bf16_t* __restrict__ d_o, const bf16_t* __restrict__ w_down, const bf16_t* g_in,
-    const bf16_t* u_in, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* dg_out,
-    bf16_t* du_out, LoraSeg lo) {
-  static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(tile_start, tile_desc, E, F / C::BN, [&](const MTile& t) {
-    f32x4 acc[C::FM][C::FN];
-    zero_acc<C>(acc);
-    const int n0 = t.nt * C::BN;
-    // B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
-    const bf16_t* bs[1] = {w_down + static_cast<int64_t>(t.e) * F * H + static_cast<int64_t>(n0) * H};
-    gemm_mainloop<C, true, true>(d_o + static_cast<int64_t>(t.m0) * H, H, t.m_lim, bs, H, F - n0, H, smem,
-                                 acc);
-    if constexpr (kLora) {
-      const bf16_t* bl[1] = {lo.b0 + (static_cast<int64_t>(t.e) * F + n0) * lo.rank};
-      gemm_mainloop<C, true, true>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, lo.rank,
-                                   F - n0, lo.rank, smem, acc);
-    }
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int mi = 0; mi < C::FM; ++mi) {
-      const int r = frag_row<C>(mi, lane);
-      if (r >= t.m_lim) continue;
-      const int64_t base = static_cast<int64_t>(t.m0 + r) * F + n0;
-#pragma unroll
-      for (int ni = 0; ni < C::FN; ++ni) {
-        const int c = frag_col<C>(ni, lane);
-        const uint2 gw = *reinterpret_cast<const uint2*>(g_in + base + c);
-        const uint2 uw = *reinterpret_cast<const uint2*>(u_in + base + c);
-        const float gv[4] = {lo_bf(gw.x), hi_bf(gw.x), lo_bf(gw.y), hi_bf(gw.y)};
-        const float uv[4] = {lo_bf(uw.x), hi_bf(uw.x), lo_bf(uw.y), hi_bf(uw.y)};
-        f32x4 dgv, duv;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float da = acc[mi][ni][i];
-          const float s = sigmoid_f(gv[i]);
-          dgv[i] = da * uv[i] * s * (1.0f + gv[i] * (1.0f - s));
-          duv[i] = da * gv[i] * s;
-        }
-        *reinterpret_cast<uint2*>(dg_out + base + c) = pack4_bf16(dgv);
-        *reinterpret_cast<uint2*>(du_out + base + c) = pack4_bf16(duv);
-      }
-    }
-  });
-}
-
-// dXp = dG W_gate[e]^T + dU W_up[e]^T  (K = 2F in two segments, N = H); with
-// kLora a third segment Q1 a1[e]^T (Q1 = scale (dG b1_gate^T + dU b1_up^T),
-// [rows][r]; a1 [E][H][r]: K-contiguous rows of the B tile).
-template <class C, bool kLora>
-__global__ __launch_bounds__(C::kThreads) void k_gateup_dgrad(
-    const bf16_t* __restrict__ dg_in, const bf16_t* __restrict__ du_in, const bf16_t* __restrict__ w_gate,
-    const bf16_t* __restrict__ w_up, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tile_start, const int2* __restrict__ tile_desc, int E, int H, int F, bf16_t* __restrict__ dxp_out,
-    LoraSeg lo) {
-  static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
-  __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(tile_start, tile_desc, E, H / C::BN, [&](const MTile& t) {
-    f32x4 acc[C::FM][C::FN];
-    zero_acc<C>(acc);
-    const int n0 = t.nt * C::BN;
-    // B(k = f, n = h) = W[e][h][f]: K-contiguous rows of W_gate / W_up.
-    const int64_t wofs = static_cast<int64_t>(t.e) * H * F + static_cast<int64_t>(n0) * F;
-    const int64_t aofs = static_cast<int64_t>(t.m0) * F;
-    const bf16_t* bg[1] = {w_gate + wofs};
-    gemm_mainloop<C, true, true>(dg_in + aofs, F, t.m_lim, bg, F, H - n0, F, smem, acc);
-    const bf16_t* bu[1] = {w_up + wofs};
-    gemm_mainloop<C, true, true>(du_in + aofs, F, t.m_lim, bu, F, H - n0, F, smem, acc);
-    if constexpr (kLora) {
-      const bf16_t* bl[1] = {lo.b0 + (static_cast<int64_t>(t.e) * H + n0) * lo.rank};
-      gemm_mainloop<C, true, true>(lo.a + static_cast<int64_t>(t.m0) * lo.rank, lo.rank, t.m_lim, bl, lo.rank,
-                                   H - n0, lo.rank, smem, acc);
-    }
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int mi = 0; mi < C::FM; ++mi) {
-      const int r = frag_row<C>(mi, lane);
-      if (r >= t.m_lim) continue;
-      const int64_t base = static_cast<int64_t>(t.m0 + r) * H + n0;
-#pragma unroll
-      for (int ni = 0; ni < C::FN; ++ni)
-        *reinterpret_cast<uint2*>(dxp_out + base + frag_col<C>(ni, lane)) = pack4_bf16(acc[mi][ni]);
     }
   });
 }
@@ -324,7 +180,7 @@ __device__ __forceinline__ bool wgrad_locate(int i, int E, int M, int N, int& e,
 
 // dW_down[e] (F x H) = A_e^T dO_e.
 template <class C_, bool F32>
-struct DownWgradJobs {
+struct DownWgradJobs : StagedCopyOut<C_, DownWgradJobs<C_, F32>> {
   using C = C_;
   const int32_t* offsets;
   const bf16_t *act, *d_o;
@@ -347,8 +203,7 @@ struct DownWgradJobs {
     j.n0 = n0;
     return true;
   }
-  // bf16 gradients leave through the LDS staging area
-  static constexpr bool kStaged = !F32;
+  static constexpr bool kStaged = !F32;  // bf16 gradients leave through the LDS staging area
   __device__ void stage_dst(const Job<C>& j, bf16_t* (&dst)[C::NB], int64_t& ld, int& rows) const {
     dst[0] = static_cast<bf16_t*>(dw_down) + static_cast<int64_t>(j.e) * F * H + static_cast<int64_t>(j.m0) * H + j.n0;
     ld = H;
@@ -368,7 +223,7 @@ struct DownWgradJobs {
 
 // dW_gate[e] = Xp_e^T dG_e, dW_up[e] = Xp_e^T dU_e  (H x F each).
 template <class C_, bool F32>
-struct GateUpWgradJobs {
+struct GateUpWgradJobs : StagedCopyOut<C_, GateUpWgradJobs<C_, F32>> {
   using C = C_;
   const int32_t* offsets;
   const bf16_t *xp, *dg_in, *du_in;
@@ -473,6 +328,317 @@ struct LoraWgradJobs {
   }
 };
 
+// ---------------------------------------------------------------- row-tile products as job streams
+// The products over each expert's rows run as job streams (gemm_stream):
+// job i of a workgroup is segment i % NSEG of logical tile
+// xcd_tile(block) + (i / NSEG) * gridDim of the tile_start[E] x n_ntiles
+// tiles (row tile from the tile table, column tile nt); the segments of a
+// tile (two halves of a K = 2F reduction, an adapter term) chain into one
+// accumulator.  The table is read through the scalar cache, and the tiles
+// leave through the LDS staging area, so the pipeline runs on across tiles.
+template <int NSEG>
+__device__ __forceinline__ bool row_job(int i, const int32_t* tile_start, const int2* tile_desc, int E, int n_ntiles,
+                                        MTile& t, int& seg) {
+  const int total = uniform_load(tile_start + E) * n_ntiles;
+  const int ti = i / NSEG;
+  const int logical = xcd_tile(blockIdx.x, gridDim.x) + ti * gridDim.x;
+  if (logical >= total) return false;
+  const int mt = logical / n_ntiles;
+  const uint64_t d = uniform_load(reinterpret_cast<const uint64_t*>(tile_desc + mt));  // {x, y}: x in the low half
+  const int dy = static_cast<int>(d >> 32);
+  t.e = dy & 0xff;
+  t.m_lim = dy >> 8;
+  t.m0 = static_cast<int>(static_cast<uint32_t>(d));
+  t.nt = logical - mt * n_ntiles;
+  seg = i - ti * NSEG;
+  return true;
+}
+
+template <class C>
+__device__ __forceinline__ void row_job_fill(Job<C>& j, const MTile& t, int n0, int n_lim) {
+  j.m_lim = t.m_lim;
+  j.n_lim = n_lim;
+  j.e = t.e;
+  j.m0 = t.m0;
+  j.n0 = n0;
+}
+
+// O = A W_down[e]  (K = F, N = H); with kLora a second segment P2 b2[e]
+// (P2 = scale A a2, [rows][r]; b2 [E][r][H], MN-contiguous like W_down).
+template <class C_, bool kLora>
+struct DownFwdJobs : StagedCopyOut<C_, DownFwdJobs<C_, kLora>> {
+  using C = C_;
+  const bf16_t *act, *w_down;
+  const int32_t* tile_start;
+  const int2* tile_desc;
+  int E, H, F;
+  bf16_t* o;
+  LoraSeg lo;
+  __device__ bool get(int i, Job<C>& j) const {
+    MTile t;
+    int seg;
+    if (!row_job<kLora ? 2 : 1>(i, tile_start, tile_desc, E, H / C::BN, t, seg)) return false;
+    const int n0 = t.nt * C::BN;
+    row_job_fill(j, t, n0, H - n0);
+    if (seg == 0) {
+      j.a = act + static_cast<int64_t>(t.m0) * F;
+      j.lda = F;
+      j.b[0] = w_down + static_cast<int64_t>(t.e) * F * H + n0;
+      j.ldb = H;
+      j.K = F;
+      j.chain = kLora;
+    } else {
+      j.a = lo.a + static_cast<int64_t>(t.m0) * lo.rank;
+      j.lda = lo.rank;
+      j.b[0] = lo.b0 + static_cast<int64_t>(t.e) * lo.rank * H + n0;
+      j.ldb = H;
+      j.K = lo.rank;
+      j.chain = false;
+    }
+    return true;
+  }
+  __device__ void stage_dst(const Job<C>& j, bf16_t* (&dst)[C::NB], int64_t& ld, int& rows) const {
+    dst[0] = o + static_cast<int64_t>(j.m0) * H + j.n0;
+    ld = H;
+    rows = j.m_lim;
+  }
+};
+
+// dXp = dG W_gate[e]^T + dU W_up[e]^T  (K = 2F as two segments, N = H); with
+// kLora a third segment Q1 a1[e]^T (Q1 = scale (dG b1_gate^T + dU b1_up^T),
+// [rows][r]; a1 [E][H][r]: K-contiguous rows of the B tile).  B(k = f,
+// n = h) = W[e][h][f]: K-contiguous rows of W_gate / W_up.
+template <class C_, bool kLora>
+struct GateUpDgradJobs : StagedCopyOut<C_, GateUpDgradJobs<C_, kLora>> {
+  using C = C_;
+  const bf16_t *dg, *du, *w_gate, *w_up;
+  const int32_t* tile_start;
+  const int2* tile_desc;
+  int E, H, F;
+  bf16_t* dxp;
+  LoraSeg lo;
+  __device__ bool get(int i, Job<C>& j) const {
+    MTile t;
+    int seg;
+    if (!row_job<kLora ? 3 : 2>(i, tile_start, tile_desc, E, H / C::BN, t, seg)) return false;
+    const int n0 = t.nt * C::BN;
+    row_job_fill(j, t, n0, H - n0);
+    if (seg < 2) {
+      const int64_t wofs = static_cast<int64_t>(t.e) * H * F + static_cast<int64_t>(n0) * F;
+      j.a = (seg == 0 ? dg : du) + static_cast<int64_t>(t.m0) * F;
+      j.lda = F;
+      j.b[0] = (seg == 0 ? w_gate : w_up) + wofs;
+      j.ldb = F;
+      j.K = F;
+      j.chain = seg == 0 || kLora;
+    } else {
+      j.a = lo.a + static_cast<int64_t>(t.m0) * lo.rank;
+      j.lda = lo.rank;
+      j.b[0] = lo.b0 + (static_cast<int64_t>(t.e) * H + n0) * lo.rank;
+      j.ldb = lo.rank;
+      j.K = lo.rank;
+      j.chain = false;
+    }
+    return true;
+  }
+  __device__ void stage_dst(const Job<C>& j, bf16_t* (&dst)[C::NB], int64_t& ld, int& rows) const {
+    dst[0] = dxp + static_cast<int64_t>(j.m0) * H + j.n0;
+    ld = H;
+    rows = j.m_lim;
+  }
+};
+
+// Staged-drain unit of the SwiGLU epilogues: 8 consecutive columns of one
+// row.  A slice gives every thread one unit: kCpr units per row, lanes
+// l / kCpr of a wave on consecutive rows.
+template <class C, int kCols>
+struct RowUnits {
+  static constexpr int kCpr = kCols / 8;
+  static constexpr int kRowsPerWave = 64 / kCpr;
+  static constexpr int kSliceRows = C::kThreads / 64 * kRowsPerWave;
+  static constexpr int kSlices = C::BM / kSliceRows;
+  static_assert(64 % kCpr == 0 && kSlices * kSliceRows == C::BM && kSlices % 2 == 0 && kSliceRows % 16 == 0,
+                "an even number of slices of 16k rows");
+  __device__ static __forceinline__ int row(int sl) {
+    return (threadIdx.x >> 6) * kRowsPerWave + (threadIdx.x & 63) / kCpr + sl * kSliceRows;
+  }
+  __device__ static __forceinline__ int chunk() { return (threadIdx.x & 63) % kCpr; }
+};
+
+__device__ __forceinline__ void unpack8(const uint4& w, float (&f)[8]) {
+  const uint32_t v[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = lo_bf(v[i]);
+    f[2 * i + 1] = hi_bf(v[i]);
+  }
+}
+__device__ __forceinline__ uint4 pack8(const float (&f)[8]) {
+  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                    pack_bf16x2(f[6], f[7]));
+}
+
+// G, U (gate/up products) and A = silu(G) U per expert, with the SwiGLU on the
+// bf16 G and U; G and U are skipped when g_out is null, A when a_out is.
+// With kLora a second segment P1 [b1_gate | b1_up][e] (P1 = scale Xp a1,
+// [rows][r]; b1 [E][r][F], MN-contiguous like W_gate).
+template <bool kLora>
+struct GateUpFwdJobs {
+  using C = GateUpFwd;
+  const bf16_t *xp, *w_gate, *w_up;
+  const int32_t* tile_start;
+  const int2* tile_desc;
+  int E, H, F;
+  bf16_t *g_out, *u_out, *a_out;
+  LoraSeg lo;
+  __device__ bool get(int i, Job<C>& j) const {
+    MTile t;
+    int seg;
+    if (!row_job<kLora ? 2 : 1>(i, tile_start, tile_desc, E, F / C::BNS, t, seg)) return false;
+    const int n0 = t.nt * C::BNS;
+    row_job_fill(j, t, n0, F - n0);
+    if (seg == 0) {
+      const int64_t wofs = static_cast<int64_t>(t.e) * H * F + n0;
+      j.a = xp + static_cast<int64_t>(t.m0) * H;
+      j.lda = H;
+      j.b[0] = w_gate + wofs;
+      j.b[1] = w_up + wofs;
+      j.ldb = F;
+      j.K = H;
+      j.chain = kLora;
+    } else {
+      const int64_t lofs = static_cast<int64_t>(t.e) * lo.rank * F + n0;
+      j.a = lo.a + static_cast<int64_t>(t.m0) * lo.rank;
+      j.lda = lo.rank;
+      j.b[0] = lo.b0 + lofs;
+      j.b[1] = lo.b1 + lofs;
+      j.ldb = F;
+      j.K = lo.rank;
+      j.chain = false;
+    }
+    return true;
+  }
+  // staged drain: one slice per call; unit (row, 8 columns) reads G (gate
+  // block) and U (up block) and stores G, U and A
+  using Units = RowUnits<C, C::BNS>;
+  static constexpr bool kStaged = true;
+  static constexpr int kDrainCalls = Units::kSlices;
+  struct Drain {
+    int64_t base;  // element offset of the tile's (0, 0) in G, U and A
+    int rows;
+  };
+  __device__ __forceinline__ void drain_reset(Drain& d) const {
+    d.base = 0;
+    d.rows = 0;
+  }
+  __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
+    d.base = static_cast<int64_t>(j.m0) * F + j.n0;
+    d.rows = j.m_lim;
+  }
+  __device__ __forceinline__ void drain(Drain& d, const char* stg, int sl) const {
+    const int s = sl < Units::kSlices ? sl : Units::kSlices - 1;
+    const int r = Units::row(s), c = Units::chunk();
+    const uint4 gw = *reinterpret_cast<const uint4*>(stg + Staged<C>::off(r, c));
+    const uint4 uw = *reinterpret_cast<const uint4*>(stg + Staged<C>::off(r, Units::kCpr + c));
+    float gv[8], uv[8], av[8];
+    unpack8(gw, gv);
+    unpack8(uw, uv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) av[i] = silu_f(gv[i]) * uv[i];
+    const uint32_t off = sl < Units::kSlices ? static_cast<uint32_t>(r * F * 2 + c * 16) : kOob;
+    const int rows_gu = g_out != nullptr ? d.rows : 0, rows_a = a_out != nullptr ? d.rows : 0;
+    buf_store16(rows_rsrc(g_out + d.base, rows_gu, F * 2, C::BNS * 2), off, gw);
+    buf_store16(rows_rsrc(u_out + d.base, rows_gu, F * 2, C::BNS * 2), off, uw);
+    buf_store16(rows_rsrc(a_out + d.base, rows_a, F * 2, C::BNS * 2), off, pack8(av));
+  }
+};
+
+// dA = dO W_down[e]^T (K = H, N = F) fused with the SwiGLU backward:
+// s = sigmoid(G); dG = dA U s (1 + G (1 - s)); dU = dA G s, with dA the
+// bf16 product.  dG and dU may overwrite G and U in place: each element of
+// G and U is read by the one thread that later writes the same element of
+// dG and dU, and by no one else.  With kLora a second segment Q2 a2[e]^T
+// (Q2 = scale dO b2^T, [rows][r]; a2 [E][F][r]: K-contiguous rows of the B
+// tile).  B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
+template <class C_, bool kLora>
+struct DownDgradJobs {
+  using C = C_;
+  const bf16_t *d_o, *w_down;
+  const bf16_t *g_in, *u_in;
+  const int32_t* tile_start;
+  const int2* tile_desc;
+  int E, H, F;
+  bf16_t *dg_out, *du_out;
+  LoraSeg lo;
+  __device__ bool get(int i, Job<C>& j) const {
+    MTile t;
+    int seg;
+    if (!row_job<kLora ? 2 : 1>(i, tile_start, tile_desc, E, F / C::BN, t, seg)) return false;
+    const int n0 = t.nt * C::BN;
+    row_job_fill(j, t, n0, F - n0);
+    if (seg == 0) {
+      j.a = d_o + static_cast<int64_t>(t.m0) * H;
+      j.lda = H;
+      j.b[0] = w_down + static_cast<int64_t>(t.e) * F * H + static_cast<int64_t>(n0) * H;
+      j.ldb = H;
+      j.K = H;
+      j.chain = kLora;
+    } else {
+      j.a = lo.a + static_cast<int64_t>(t.m0) * lo.rank;
+      j.lda = lo.rank;
+      j.b[0] = lo.b0 + (static_cast<int64_t>(t.e) * F + n0) * lo.rank;
+      j.ldb = lo.rank;
+      j.K = lo.rank;
+      j.chain = false;
+    }
+    return true;
+  }
+  // staged drain: one slice per call; unit (row, 8 columns) of dA, whose G
+  // and U were loaded by the previous call (or the setup)
+  using Units = RowUnits<C, C::BN>;
+  static constexpr bool kStaged = true;
+  static constexpr int kDrainCalls = Units::kSlices;
+  struct Drain {
+    int64_t base;  // element offset of the tile's (0, 0) in G, U, dG and dU
+    int rows;
+    uint4 gw, uw;  // G and U of the next call's unit
+  };
+  __device__ __forceinline__ void drain_reset(Drain& d) const {
+    d.base = 0;
+    d.rows = 0;
+    d.gw = d.uw = make_uint4(0, 0, 0, 0);
+  }
+  __device__ __forceinline__ uint32_t unit_off(int sl) const {
+    return sl < Units::kSlices ? static_cast<uint32_t>(Units::row(sl) * F * 2 + Units::chunk() * 16) : kOob;
+  }
+  __device__ __forceinline__ void prefetch(Drain& d, int sl) const {
+    d.gw = buf_load16(rows_rsrc(g_in + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl));
+    d.uw = buf_load16(rows_rsrc(u_in + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl));
+  }
+  __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
+    d.base = static_cast<int64_t>(j.m0) * F + j.n0;
+    d.rows = j.m_lim;
+    prefetch(d, 0);
+  }
+  __device__ __forceinline__ void drain(Drain& d, const char* stg, int sl) const {
+    const int s = sl < Units::kSlices ? sl : Units::kSlices - 1;
+    const int r = Units::row(s), c = Units::chunk();
+    float da[8], gv[8], uv[8], dgv[8], duv[8];
+    unpack8(*reinterpret_cast<const uint4*>(stg + Staged<C>::off(r, c)), da);
+    unpack8(d.gw, gv);
+    unpack8(d.uw, uv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float sg = sigmoid_f(gv[i]);
+      dgv[i] = da[i] * uv[i] * sg * (1.0f + gv[i] * (1.0f - sg));
+      duv[i] = da[i] * gv[i] * sg;
+    }
+    buf_store16(rows_rsrc(dg_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(dgv));
+    buf_store16(rows_rsrc(du_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(duv));
+    prefetch(d, sl + 1);
+  }
+};
+
 // One persistent kernel for every product: the job provider decides.
 template <class P, bool A_KC, bool B_KC>
 __global__ __launch_bounds__(P::C::kThreads) void k_stream(P prov) {
@@ -536,66 +702,70 @@ void run_stream(const P& prov, int64_t max_jobs, int kid, hipStream_t s) {
 
 template <class C>
 void down_fwd(const ExpertArgs& a, bf16_t* o, hipStream_t s) {
-  const bool lora = a.lora.rank > 0;
-  auto k = lora ? k_down_fwd<C, true> : k_down_fwd<C, false>;
   LoraSeg lo;
-  if (lora) {
+  if (a.lora.rank > 0) {
     lo.a = a.lora.p2;
     lo.b0 = a.lora.b2;
     lo.rank = a.lora.rank;
   }
-  const int grid =
-      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
-  TraceScope trace_scope(K_DOWN_FWD, s);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.act, a.w_down, a.offsets, a.tile_start, a.tile_desc, a.E,
-                     a.H, a.F, o, lo);
+  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN);
+  if (lo.rank > 0)
+    run_stream<true, false>(DownFwdJobs<C, true>{{}, a.act, a.w_down, a.tile_start, a.tile_desc, a.E, a.H, a.F, o, lo},
+                            tiles, K_DOWN_FWD, s);
+  else
+    run_stream<true, false>(DownFwdJobs<C, false>{{}, a.act, a.w_down, a.tile_start, a.tile_desc, a.E, a.H, a.F, o, lo},
+                            tiles, K_DOWN_FWD, s);
 }
 
 template <class C>
 void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, const bf16_t* q2, hipStream_t s) {
-  const bool lora = q2 != nullptr;
-  auto k = lora ? k_down_dgrad_swiglu<C, true> : k_down_dgrad_swiglu<C, false>;
   LoraSeg lo;
-  if (lora) {
+  if (q2 != nullptr) {
     lo.a = q2;
     lo.b0 = a.lora.a2;
     lo.rank = a.lora.rank;
   }
-  const int grid =
-      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN));
-  TraceScope trace_scope(K_DOWN_DGRAD, s);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, d_o, a.w_down, a.g, a.u, a.offsets, a.tile_start,
-                     a.tile_desc, a.E, a.H, a.F, dg, du, lo);
+  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN);
+  if (lo.rank > 0)
+    run_stream<true, true>(DownDgradJobs<C, true>{d_o, a.w_down, a.g, a.u, a.tile_start, a.tile_desc, a.E, a.H, a.F,
+                                                  dg, du, lo},
+                           tiles, K_DOWN_DGRAD, s);
+  else
+    run_stream<true, true>(DownDgradJobs<C, false>{d_o, a.w_down, a.g, a.u, a.tile_start, a.tile_desc, a.E, a.H, a.F,
+                                                   dg, du, lo},
+                           tiles, K_DOWN_DGRAD, s);
 }
 
 template <class C>
 void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_t* dxp, const bf16_t* q1,
                   hipStream_t s) {
-  const bool lora = q1 != nullptr;
-  auto k = lora ? k_gateup_dgrad<C, true> : k_gateup_dgrad<C, false>;
   LoraSeg lo;
-  if (lora) {
+  if (q1 != nullptr) {
     lo.a = q1;
     lo.b0 = a.lora.a1;
     lo.rank = a.lora.rank;
   }
-  const int grid =
-      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN));
-  TraceScope trace_scope(K_GATEUP_DGRAD, s);
-  hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, dg, du, a.w_gate, a.w_up, a.offsets, a.tile_start,
-                     a.tile_desc, a.E, a.H, a.F, dxp, lo);
+  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.H / C::BN);
+  if (lo.rank > 0)
+    run_stream<true, true>(GateUpDgradJobs<C, true>{{}, dg, du, a.w_gate, a.w_up, a.tile_start, a.tile_desc, a.E, a.H,
+                                                    a.F, dxp, lo},
+                           tiles, K_GATEUP_DGRAD, s);
+  else
+    run_stream<true, true>(GateUpDgradJobs<C, false>{{}, dg, du, a.w_gate, a.w_up, a.tile_start, a.tile_desc, a.E,
+                                                     a.H, a.F, dxp, lo},
+                           tiles, K_GATEUP_DGRAD, s);
 }
 
 template <class C, bool F32>
 void down_wgrad(const ExpertArgs& a, const bf16_t* d_o, void* dw_down, hipStream_t s) {
-  DownWgradJobs<C, F32> p{a.offsets, a.act, d_o, a.E, a.H, a.F, dw_down};
+  DownWgradJobs<C, F32> p{{}, a.offsets, a.act, d_o, a.E, a.H, a.F, dw_down};
   run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.F / C::BM) * (a.H / C::BNS), K_DOWN_WGRAD, s);
 }
 
 template <class C, bool F32>
 void gateup_wgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate, void* dw_up,
                   hipStream_t s) {
-  GateUpWgradJobs<C, F32> p{a.offsets, a.xp, dg, du, a.E, a.H, a.F, dw_gate, dw_up};
+  GateUpWgradJobs<C, F32> p{{}, a.offsets, a.xp, dg, du, a.E, a.H, a.F, dw_gate, dw_up};
   run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.H / C::BM) * (a.F / C::BNS), K_GATEUP_WGRAD, s);
 }
 
@@ -616,23 +786,31 @@ void gateup_wgrad_any(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, v
 
 hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute) {
   using C = GateUpFwd;
-  const bool lora = a.lora.rank > 0;
-  auto k = a.xp_rows != nullptr ? k_gateup_fwd<true, false>
-                                : (lora ? k_gateup_fwd<false, true> : k_gateup_fwd<false, false>);
+  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS);
+  const int kid = recompute ? K_GATEUP_RECOMPUTE : K_GATEUP_FWD;
+  if (a.xp_rows != nullptr) {  // rows read through an index: one pipeline per tile
+    auto k = k_gateup_fwd_rows;
+    const int grid = persistent_grid(k, C::kThreads, tiles);
+    TraceScope trace_scope(kid, s);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.xp_rows, a.xp_bytes, a.w_gate, a.w_up,
+                       a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g, a.u, a.act);
+    return hipGetLastError();
+  }
   LoraSeg lo;
-  if (lora) {
+  if (a.lora.rank > 0) {
     lo.a = a.lora.p1;
     lo.b0 = a.lora.b1_gate;
     lo.b1 = a.lora.b1_up;
     lo.rank = a.lora.rank;
   }
-  const int grid =
-      persistent_grid(k, C::kThreads, static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BNS));
-  {
-    TraceScope trace_scope(recompute ? K_GATEUP_RECOMPUTE : K_GATEUP_FWD, s);
-    hipLaunchKernelGGL(k, dim3(grid), dim3(C::kThreads), 0, s, a.xp, a.xp_rows, a.xp_bytes, a.w_gate, a.w_up,
-                       a.offsets, a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g, a.u, a.act, lo);
-  }
+  if (lo.rank > 0)
+    run_stream<true, false>(GateUpFwdJobs<true>{a.xp, a.w_gate, a.w_up, a.tile_start, a.tile_desc, a.E, a.H, a.F, a.g,
+                                                a.u, a.act, lo},
+                            tiles, kid, s);
+  else
+    run_stream<true, false>(GateUpFwdJobs<false>{a.xp, a.w_gate, a.w_up, a.tile_start, a.tile_desc, a.E, a.H, a.F,
+                                                 a.g, a.u, a.act, lo},
+                            tiles, kid, s);
   return hipGetLastError();
 }
 

@@ -409,32 +409,44 @@ __device__ __forceinline__ uint2 pack4_bf16(const f32x4& v) {
   return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
 
+template <class C>
+struct Job {
+  const bf16_t* a;
+  int64_t lda;
+  int m_lim;
+  const bf16_t* b[C::NB];
+  int64_t ldb;
+  int n_lim;
+  int K;       // valid k; 0 = an empty tile (its epilogue sees zeros)
+  bool chain;  // the next job continues this tile
+  int e, m0, n0;
+};
+
 // ---------------------------------------------------------------- staged output
 // A job provider that declares `static constexpr bool kStaged = true` hands
 // its finished tiles over as bf16 through LDS instead of storing them from
 // the accumulators: after a tile's last K step the workgroup writes the tile
-// into an LDS staging area, and each following K step stores one slice of it
-// (one 16-byte chunk per thread) to global memory.  The stores then overlap
-// the next tile's MFMAs; stored straight from the accumulators they stall
-// every wave at the tile boundary until they complete (one counter tracks
-// both loads and stores), which costs as much as the tile's MFMAs when the
-// reduction is short (weight gradients over one expert's rows).
-// P::stage_dst(job, dst, ld, rows) names the NB destinations (element (0, 0)
-// of each BM x BNS block, row pitch ld elements, `rows` valid rows); whole
-// rows of BNS columns are written.
+// into an LDS staging area, and the first step of each following pair of K
+// steps drains part of it to global memory (P::drain, with any elementwise
+// epilogue), so that the stores overlap the next tile's MFMAs.  Stored
+// straight from the accumulators they stall every wave at the tile boundary
+// until they complete (one counter tracks both loads and stores), which costs
+// as much as the tile's MFMAs when the reduction is short (weight gradients
+// over one expert's rows).  The provider supplies
+//   Drain                          per-thread state of the tile being drained
+//   kDrainCalls                    drain calls per tile
+//   drain_setup(job, Drain&)       once the tile is staged
+//   drain(Drain&, staging, p)      call p (p >= kDrainCalls: no memory effect)
+//   drain_reset(Drain&)            a state whose calls touch no memory
+// A tile whose successor is shorter than kDrainCalls step pairs is drained
+// in full before the successor is staged.
+// Staging layout: tile row r (BN bf16, all NB blocks side by side), 16-byte
+// chunk q at Staged<C>::off(r, q).
 template <class C>
 struct Staged {
-  static constexpr int kRowBytes = C::BN * 2;                   // one tile row, all NB blocks
-  static constexpr int kBytes = C::BM * kRowBytes;              // LDS staging area
-  static constexpr int kCpr = C::BNS * 2 / 16;                  // 16-byte chunks per block row
-  static constexpr int kRowsPerWave = 64 / kCpr;                // block rows one wave stores per slice
-  static constexpr int kWavesPerDst = C::kThreads / 64 / C::NB;
-  static constexpr int kSliceRows = kWavesPerDst * kRowsPerWave;
-  static constexpr int kSlices = C::BM / kSliceRows;
-  static constexpr int kXor = (C::BN / 8 < 16 ? C::BN / 8 : 16) - 1;  // chunk swizzle: rows of 16 hit distinct banks
-  static_assert(64 % kCpr == 0 && (C::kThreads / 64) % C::NB == 0, "a wave stores whole block rows of one block");
-  static_assert(kSlices * kSliceRows == C::BM && kSliceRows % 16 == 0, "slices of 16k rows keep the swizzle fixed");
-  // byte offset of chunk q (0 .. BN/8) of tile row r in the staging area
+  static constexpr int kRowBytes = C::BN * 2;                         // one tile row, all NB blocks
+  static constexpr int kBytes = C::BM * kRowBytes;                    // LDS staging area
+  static constexpr int kXor = (C::BN / 8 < 16 ? C::BN / 8 : 16) - 1;  // rows of 16 hit distinct banks
   static __device__ __forceinline__ int off(int r, int q) { return r * kRowBytes + ((q ^ (r & kXor)) << 4); }
 };
 
@@ -453,17 +465,90 @@ __device__ __forceinline__ void buf_store16(__amdgpu_buffer_rsrc_t r, uint32_t o
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), r, static_cast<int>(off), 0, 0);
 }
 
+// Buffer resource over `rows` rows of `width_bytes` at pitch ld_bytes:
+// accesses to rows >= rows fall outside it (stores are dropped, loads read
+// zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, int rows, int64_t ld_bytes,
+                                                            int width_bytes) {
+  return make_rsrc(base, rows > 0 ? static_cast<int64_t>(rows - 1) * ld_bytes + width_bytes : 0);
+}
+
+// Drain that copies the staged tile to NB destinations (element (0, 0) of
+// each BM x BNS block, pitch ld elements, `rows` valid rows; whole rows of BNS
+// columns are written).  A slice is one 16-byte chunk per thread: wave w
+// stores block w % NB, kRowsPerWave rows of it per slice.
 template <class C>
-struct Job {
-  const bf16_t* a;
-  int64_t lda;
-  int m_lim;
-  const bf16_t* b[C::NB];
-  int64_t ldb;
-  int n_lim;
-  int K;       // valid k; 0 = an empty tile (its epilogue sees zeros)
-  bool chain;  // the next job continues this tile
-  int e, m0, n0;
+struct StagedCopy {
+  using SO = Staged<C>;
+  static constexpr int kCpr = C::BNS * 2 / 16;  // chunks per block row
+  static constexpr int kRowsPerWave = 64 / kCpr;
+  static constexpr int kSliceRows = C::kThreads / 64 / C::NB * kRowsPerWave;
+  static constexpr int kSlices = C::BM / kSliceRows;
+  static constexpr int kCalls = kSlices / 2;  // two slices per drain call
+  static_assert(64 % kCpr == 0 && (C::kThreads / 64) % C::NB == 0, "a wave stores whole block rows of one block");
+  static_assert(kSlices * kSliceRows == C::BM && kSlices % 2 == 0 && kSliceRows % 16 == 0,
+                "an even number of slices of 16k rows (the swizzle repeats every 16 rows)");
+  struct State {
+    __amdgpu_buffer_rsrc_t out;
+    uint32_t ld;  // bytes
+  };
+  __device__ static __forceinline__ void reset(State& d) {
+    d.out = make_rsrc(nullptr, 0);
+    d.ld = 0;
+  }
+  __device__ static __forceinline__ void setup(State& d, bf16_t* const (&dst)[C::NB], int64_t ld, int rows) {
+    const int h = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) % C::NB;
+    bf16_t* o = dst[0];
+#pragma unroll
+    for (int i = 1; i < C::NB; ++i) o = h == i ? dst[i] : o;
+    d.out = rows_rsrc(o, rows, ld * 2, C::BNS * 2);
+    d.ld = static_cast<uint32_t>(ld * 2);
+  }
+  __device__ static __forceinline__ void slice(const State& d, const char* stg, int sl) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int cq = lane % kCpr;
+    const int row0 = (wv / C::NB) * kRowsPerWave + lane / kCpr;  // row within the slice
+    const int s = sl < kSlices ? sl : kSlices - 1;
+    const uint4 v = *reinterpret_cast<const uint4*>(stg + SO::off(row0, (wv % C::NB) * kCpr + cq) +
+                                                    s * (kSliceRows * SO::kRowBytes));
+    const uint32_t off = static_cast<uint32_t>(row0 + s * kSliceRows) * d.ld + cq * 16;
+    buf_store16(d.out, sl < kSlices ? off : kOob, v);
+  }
+  __device__ static __forceinline__ void call(const State& d, const char* stg, int p) {  // two slices
+    slice(d, stg, 2 * p);
+    slice(d, stg, 2 * p + 1);
+  }
+};
+
+// Mixin for providers whose staged tiles are copied out unchanged; Derived
+// supplies stage_dst(job, dst, ld, rows).
+template <class C, class Derived>
+struct StagedCopyOut {
+  static constexpr bool kStaged = true;
+  using Drain = typename StagedCopy<C>::State;
+  static constexpr int kDrainCalls = StagedCopy<C>::kCalls;
+  __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
+    bf16_t* dst[C::NB];
+    int64_t ld;
+    int rows;
+    static_cast<const Derived*>(this)->stage_dst(j, dst, ld, rows);
+    StagedCopy<C>::setup(d, dst, ld, rows);
+  }
+  __device__ __forceinline__ void drain(Drain& d, const char* stg, int p) const { StagedCopy<C>::call(d, stg, p); }
+  __device__ __forceinline__ void drain_reset(Drain& d) const { StagedCopy<C>::reset(d); }
+};
+
+
+// The drain interface of a staged provider, or nothing.
+template <class P, bool kStaged>
+struct DrainOf {
+  struct type {};
+  static constexpr int kCalls = 0;
+};
+template <class P>
+struct DrainOf<P, true> {
+  using type = typename P::Drain;
+  static constexpr int kCalls = P::kDrainCalls;
 };
 
 // Runs every job of this workgroup (P::get(i, job) fills the i-th, false past
@@ -476,7 +561,6 @@ template <class C, bool A_KC, bool B_KC, class P>
 __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   static_assert(std::is_same<C, typename P::C>::value, "the provider's tile shape");
   constexpr bool kStaged = staged_provider<P>::value;
-  using SO = Staged<C>;
   using LA = Loader<A_KC, C::BM, C::BM, C::kThreads>;
   using LB = Loader<B_KC, C::BNS, C::BN, C::kThreads>;
   using S0 = std::integral_constant<int, 0>;
@@ -530,52 +614,38 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     for (int i = 0; i < C::NB; ++i) lb[i].store(rb[S][i], stage + C::kABytes, i * C::BNS, tid);
   };
 
-  // staged output (kStaged): this thread's chunk of every slice, the current
-  // destination and the next slice to store (kSlices: none pending)
+  // staged output (kStaged): the provider's drain state and the next drain
+  // call (kCalls: nothing pending)
   char* const stg = smem + C::kLds;
-  int d_lds = 0, d_row = 0, d_col = 0;
-  if constexpr (kStaged) {
-    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int h = wv % C::NB, cq = lane % SO::kCpr;
-    d_row = (wv / C::NB) * SO::kRowsPerWave + lane / SO::kCpr;
-    d_col = cq * 16;
-    d_lds = SO::off(d_row, h * SO::kCpr + cq);
-  }
-  __amdgpu_buffer_rsrc_t d_rsrc = make_rsrc(nullptr, 0);
-  uint32_t d_ld = 0;
-  int d_slice = SO::kSlices;
-  auto drain_one = [&](int slice) {  // slice < kSlices stores, else nothing (a branch-free no-op)
-    const int sl = slice < SO::kSlices ? slice : SO::kSlices - 1;
-    const uint4 v = *reinterpret_cast<const uint4*>(stg + d_lds + sl * (SO::kSliceRows * SO::kRowBytes));
-    const uint32_t off = static_cast<uint32_t>(d_row + sl * SO::kSliceRows) * d_ld + d_col;
-    buf_store16(d_rsrc, slice < SO::kSlices ? off : kOob, v);
+  typename DrainOf<P, kStaged>::type dr;
+  if constexpr (kStaged) prov.drain_reset(dr);
+  constexpr int kCalls = DrainOf<P, kStaged>::kCalls;
+  int d_call = kCalls;
+  auto drain_next = [&]() {
+    if constexpr (kStaged) prov.drain(dr, stg, d_call);
+  };
+  auto drain_rest = [&]() {
+    if constexpr (kStaged)
+      for (; d_call < kCalls; ++d_call) prov.drain(dr, stg, d_call);
   };
   auto finish = [&](const Job<C>& j) {  // a finished tile: epilogue, or into the staging area
     if constexpr (kStaged) {
-      if (d_slice < SO::kSlices) {  // the previous tile is not fully stored yet (short K)
-        for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
+      if (d_call < kCalls) {  // the previous tile is not fully drained yet (short K)
+        drain_rest();
         lds_barrier();
       }
-      const int wv = tid >> 6;
-      const int wm_ = wv / C::WN;
+      const int wm_ = (tid >> 6) / C::WN;
 #pragma unroll
       for (int mi = 0; mi < C::FM; ++mi) {
         const int r = wm_ * (C::BM / C::WM) + mi * 16 + (lane & 15);
 #pragma unroll
         for (int ni = 0; ni < C::FN; ++ni) {
           const int c = frag_col<C>(ni, lane);
-          *reinterpret_cast<uint2*>(stg + SO::off(r, c >> 3) + (c & 7) * 2) = pack4_bf16(acc[mi][ni]);
+          *reinterpret_cast<uint2*>(stg + Staged<C>::off(r, c >> 3) + (c & 7) * 2) = pack4_bf16(acc[mi][ni]);
         }
       }
-      bf16_t* dst[C::NB];
-      int64_t ld;
-      int rows;
-      prov.stage_dst(j, dst, ld, rows);
-      const int h = __builtin_amdgcn_readfirstlane(tid >> 6) % C::NB;
-      const int64_t bytes = rows > 0 ? static_cast<int64_t>(rows - 1) * ld * 2 + C::BNS * 2 : 0;
-      d_rsrc = make_rsrc(dst[h], bytes);
-      d_ld = static_cast<uint32_t>(ld * 2);
-      d_slice = 0;
+      prov.drain_setup(j, dr);
+      d_call = 0;
       lds_barrier();
     } else {
       prov.epilogue(j, acc);
@@ -620,12 +690,13 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     const char* cur = smem + S * C::kStage;
     char* nxt = smem + (1 - S) * C::kStage;
     uint4 af0[C::FM], bf0[C::FN], af1[C::FM], bf1[C::FN];
-    // staged output: two slices in the first step of each pair; their stores
-    // then have two steps to complete before a wait for later loads needs them
-    constexpr int kDrain = kStaged && S == 0 ? 2 : 0;
-    if constexpr (kDrain > 0) {
-      drain_one(d_slice);
-      drain_one(d_slice + 1);
+    // staged output: one drain call in the first step of each pair while
+    // the staged tile lasts, before the step's fragment reads (a fence keeps
+    // it out of the interleave, where every register is taken)
+    constexpr bool kDrain = kStaged && S == 0;
+    if constexpr (kDrain) {
+      if (d_call < kCalls) drain_next();
+      __builtin_amdgcn_sched_barrier(0);
     }
     read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 0, lane, af0, bf0);
     read_frags<C, A_KC, B_KC>(cur, cur + C::kABytes, wm, wn, 1, lane, af1, bf1);
@@ -633,20 +704,16 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     mfmas<C>(af1, bf1, acc);
     store(Other{}, nxt);
     load(Other{});
-    __builtin_amdgcn_sched_group_barrier(0x100, kReads + kDrain, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
     interleave<kMfma, kReads, 0x100, 0, 0x200>();
     interleave<kMfma, kWrites, 0x200, kLoads, 0x020>();
-    if constexpr (kDrain > 0) {
-      __builtin_amdgcn_sched_group_barrier(0x040, kDrain, 0);  // the staged slices' stores
-      d_slice = d_slice + kDrain < SO::kSlices ? d_slice + kDrain : SO::kSlices;
-    }
+    if constexpr (kDrain) d_call = d_call < kCalls ? d_call + 1 : kCalls;
     lds_barrier();
     lnext();
   };
 
   if (!cok) {  // only empty jobs: the last of them may still be staged
-    if constexpr (kStaged)
-      for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
+    drain_rest();
     return;
   }
   load(S0{});
@@ -665,8 +732,7 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     cadvance();
     if (!cok) break;
   }
-  if constexpr (kStaged)
-    for (; d_slice < SO::kSlices; ++d_slice) drain_one(d_slice);
+  drain_rest();
   lds_barrier();  // the workgroup's LDS is free again
 }
 

@@ -96,11 +96,16 @@ def test_tiny_workload_fwd_bwd():
 
 
 def test_tiny_workload_fp32_weight_grads():
+    """fp32 weight gradients skip the output rounding, so they are held to
+    1e-2 rather than 2e-2.  Their inputs are still bf16: A = silu(G) U is
+    formed from the bf16-rounded G and U (the stored activations, which the
+    backward also reads) and rounded again, up to 3 x 2^-9 relative per
+    element of A, and dO carries its own bf16 rounding."""
     inp = workloads.make("tiny")
     f, b = oracle_run(inp)
     g = gpu_run(inp, dw_fp32=True)
     for n in ("dw_r", "dw_gate", "dw_up", "dw_down"):
-        assert_close(n, g[n], b[n], tol=5e-3)
+        assert_close(n, g[n], b[n], tol=1e-2)
 
 
 EDGE = {
