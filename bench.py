@@ -72,7 +72,12 @@ def short_kernel_name(name):
     """rocprofv3 kernel name -> the library's trace name."""
     m = re.search(r"k_stream<[^>]*?::(\w+)Jobs", name)
     if m:
-        return {"DownWgrad": "down_wgrad", "GateUpWgrad": "gateup_wgrad"}.get(m.group(1), m.group(1))
+        base = {"DownWgrad": "down_wgrad", "GateUpWgrad": "gateup_wgrad", "GateUpFwd": "gateup_fwd",
+                "DownFwd": "down_fwd", "DownDgrad": "down_dgrad_swiglu", "GateUpDgrad": "gateup_dgrad",
+                "LoraWgrad": "lora_wgrad"}.get(m.group(1), m.group(1))
+        # the adapter (rank-r) variants of the row-grouped products
+        lora = re.search(r"(?:Fwd|Dgrad)Jobs<(?:[^<>]*<[^<>]*>, )?true>", name) is not None
+        return base + ("_lora" if lora else "")
     m = re.search(r"k_(\w+?)(?:<|\(|$)", name)
     if m:
         return m.group(1)
