@@ -724,11 +724,17 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   lds_barrier();
   load(S0{});
   lnext();
-  for (;;) {  // cok holds here (checked above); every exit is a break
+  // Steps alternate S0, S1.  When the jobs run out after an S0 step, one more
+  // S1 step runs on the disabled loaders (zeros, no memory access) and its
+  // accumulation is dropped: every path back to S0 then passes through S1,
+  // and the compiler's waits in S0 count S1's loads as in flight (an exit
+  // after S0 left an edge to the loop head that skipped S1, and S0 waited
+  // for loads issued one step earlier instead of two).
+  for (;;) {  // cok holds here (checked above)
     step(S0{});
     cadvance();
-    if (!cok) break;
     step(S1{});
+    if (!cok) break;
     cadvance();
     if (!cok) break;
   }
