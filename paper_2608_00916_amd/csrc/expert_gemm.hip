@@ -165,12 +165,13 @@ __device__ __forceinline__ void store4(void* out, int64_t idx, const f32x4& v) {
 // Weight-gradient jobs: expert e, rows [m0, m0+BM), columns [n0, n0+BNS) of
 // each of the NB gradients (M x N each), K = rows of the expert (0 rows:
 // the tile is written as zeros).  Workgroup job i is logical tile
-// xcd_tile(block) + i * gridDim of E x (M/BM) x (N/BNS).
+// xcd_run(i, .) of E x (M/BM) x (N/BNS): each XCD works through whole
+// experts, whose rows (the K of every tile of an expert) then stay in its L2.
 template <class C>
 __device__ __forceinline__ bool wgrad_locate(int i, int E, int M, int N, int& e, int& m0, int& n0) {
   const int nm = M / C::BM, nn = N / C::BNS;
-  const int logical = xcd_tile(blockIdx.x, gridDim.x) + i * gridDim.x;
-  if (logical >= E * nm * nn) return false;
+  const int logical = xcd_run(i, E * nm * nn);
+  if (logical < 0) return false;
   e = logical / (nm * nn);
   const int rem = logical - e * nm * nn;
   m0 = (rem / nn) * C::BM;
@@ -331,8 +332,9 @@ struct LoraWgradJobs {
 // ---------------------------------------------------------------- row-tile products as job streams
 // The products over each expert's rows run as job streams (gemm_stream):
 // job i of a workgroup is segment i % NSEG of logical tile
-// xcd_tile(block) + (i / NSEG) * gridDim of the tile_start[E] x n_ntiles
-// tiles (row tile from the tile table, column tile nt); the segments of a
+// xcd_run(i / NSEG, .) of the tile_start[E] x n_ntiles tiles (row tile from
+// the tile table, column tile nt: each XCD works through a contiguous run of
+// row tiles, so an expert's weights are fetched into one L2); the segments of a
 // tile (two halves of a K = 2F reduction, an adapter term) chain into one
 // accumulator.  The table is read through the scalar cache, and the tiles
 // leave through the LDS staging area, so the pipeline runs on across tiles.

@@ -751,6 +751,20 @@ __device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
   return (bid & 7) * per + (bid >> 3);
 }
 
+// Tile of job i of this workgroup when each XCD takes one contiguous run of
+// the `total` tiles over the whole launch: the n workgroups of XCD x take
+// tiles x * per + j + i * n (j their index on the XCD, per = ceil(total / 8)),
+// so the operands of neighbouring tiles (one expert's) are fetched into one
+// L2 rather than into every XCD's.  -1 past this XCD's run.  nblocks % 8 == 0.
+__device__ __forceinline__ int xcd_run(int i, int total) {
+  const int n = gridDim.x >> 3;
+  const int per = (total + 7) >> 3;
+  const int r = static_cast<int>(blockIdx.x >> 3) + i * n;
+  if (r >= per) return -1;
+  const int t = static_cast<int>(blockIdx.x & 7) * per + r;
+  return t < total ? t : -1;
+}
+
 // Largest e in [0, E) with tile_start[e] <= mt, or -1 if mt >= tile_start[E].
 __device__ __forceinline__ int find_group(const int32_t* tile_start, int E, int mt) {
   if (mt >= tile_start[E]) return -1;
