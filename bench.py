@@ -213,6 +213,43 @@ def lora_step(moe, t, tm, T, H, E, F, k, Tv, rank, steps, warmup):
             "ms_per_step": ms, "steps": steps}
 
 
+def ep_share_step(moe, steps, warmup):
+    """One expert-parallel rank's share on its own (the ep_share workload: 16
+    local experts, 8192 rows already grouped by expert): moe_experts_fwd +
+    moe_experts_bwd, timed after the other regions."""
+    import torch
+    import workloads
+    inp = workloads.make("ep_share")
+    d = inp["dims"]
+    R, H, E, F = d["R"], d["H"], d["E"], d["F"]
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+    t = {n: dev(inp[n]) for n in ("xp", "w_gate", "w_up", "w_down", "d_o")}
+    counts = torch.from_numpy(inp["counts"]).cuda()
+    ex = moe.MoEExperts(R, H, E, F)
+
+    def run():
+        ex.forward(t["xp"], counts, t["w_gate"], t["w_up"], t["w_down"])
+        ex.backward(t["xp"], t["w_gate"], t["w_up"], t["w_down"], t["d_o"])
+
+    for _ in range(warmup):
+        run()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(f"[bench] EP share (16 local experts, {R} rows) fwd+bwd: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    return {"entry": "moe_experts_fwd + moe_experts_bwd", "workload": "ep_share", "rows": R, "local_experts": E,
+            "rows_per_s": R / (ms * 1e-3), "ms_per_step": ms, "steps": steps,
+            "tflops": 18.0 * H * F * R / (ms * 1e-3) / 1e12}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -225,7 +262,7 @@ def main():
     ap.add_argument("--no-trace", action="store_true",
                     help="skip the kernel region (per-kernel events, roofline)")
     ap.add_argument("--no-forward-only", action="store_true",
-                    help="skip the forward-only (moe_infer) and expert-LoRA timings")
+                    help="skip the forward-only (moe_infer), expert-LoRA and EP-share timings")
     ap.add_argument("--lora-rank", type=int, default=16, help="rank of the expert-LoRA timing")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one torch copy of MIB MiB before the steps (counter calibration)")
@@ -332,6 +369,7 @@ def main():
                                                                      args.warmup)
     lora = None if args.no_forward_only else lora_step(moe, t, tm, T, H, E, F, k, Tv, args.lora_rank,
                                                        args.steps, args.warmup)
+    ep = None if args.no_forward_only else ep_share_step(moe, args.steps, args.warmup)
 
     gemm_flop = 18.0 * H * F * R
     router_flop = 6.0 * H * E * Tv
@@ -356,6 +394,7 @@ def main():
         "timing": timing,
         "forward_only": forward_only,
         "expert_lora": lora,
+        "ep_share": ep,
     }
     if traced_ms is not None:
         out["kernel_region_ms_per_step"] = traced_ms
