@@ -94,13 +94,13 @@ struct LoadKc {
   static constexpr int kPer = ROWS * (BK / 8) / kThreads;
   static_assert(kPer * kThreads == ROWS * (BK / 8), "tile rows must split evenly over the threads");
   const char* base;
-  int64_t valid;  // bytes of the r_lim valid rows
-  int64_t ld2;    // row pitch in bytes
+  int32_t valid;  // bytes of the valid rows within the tile's ROWS (< 2^31)
+  int32_t ld2;    // row pitch in bytes
   uint32_t off[kPer];
   __device__ __forceinline__ void init(const bf16_t* src, int64_t ld, int r_lim, int tid) {
     base = reinterpret_cast<const char*>(src);
-    ld2 = ld * 2;
-    valid = r_lim > 0 ? static_cast<int64_t>(r_lim) * ld2 : 0;
+    ld2 = static_cast<int32_t>(ld * 2);
+    valid = r_lim > 0 ? (r_lim < ROWS ? r_lim : ROWS) * ld2 : 0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int q = i * kThreads + tid;
@@ -112,8 +112,8 @@ struct LoadKc {
   __device__ __forceinline__ void init_rows(const bf16_t* src, int64_t ld, const int32_t* rows, int r_lim,
                                             int64_t bytes, int tid) {
     base = reinterpret_cast<const char*>(src);
-    ld2 = ld * 2;
-    valid = bytes;
+    ld2 = static_cast<int32_t>(ld * 2);
+    valid = static_cast<int32_t>(bytes);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int q = i * kThreads + tid;
@@ -151,11 +151,11 @@ struct LoadMn {
   static_assert(kPer * kThreads == BK * kUnits, "tile columns must split evenly over the threads");
   const char* base;
   int64_t valid;  // bytes of the K valid k-rows
-  int64_t ld2;
+  int32_t ld2;    // row pitch in bytes
   uint32_t off[kPer];
   __device__ __forceinline__ void init(const bf16_t* src, int64_t ld, int r_lim, int K, int tid) {
     base = reinterpret_cast<const char*>(src);
-    ld2 = ld * 2;
+    ld2 = static_cast<int32_t>(ld * 2);
     valid = K > 0 ? static_cast<int64_t>(K) * ld2 : 0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
@@ -166,7 +166,7 @@ struct LoadMn {
   }
   __device__ __forceinline__ void disable() { valid = 0; }
   __device__ __forceinline__ void load(uint4 (&v)[kPer], int kt, int, int) const {
-    const int64_t step = static_cast<int64_t>(kt) * BK * ld2;
+    const int64_t step = static_cast<int64_t>(kt) * BK * ld2;  // 64-bit: K rows can span more than 2^31 bytes
     const __amdgpu_buffer_rsrc_t r = make_rsrc(base + step, valid - step);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) v[i] = buf_load16(r, off[i]);
