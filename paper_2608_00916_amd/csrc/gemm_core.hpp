@@ -765,16 +765,4 @@ __device__ __forceinline__ int xcd_run(int i, int total) {
   return t < total ? t : -1;
 }
 
-// Largest e in [0, E) with tile_start[e] <= mt, or -1 if mt >= tile_start[E].
-__device__ __forceinline__ int find_group(const int32_t* tile_start, int E, int mt) {
-  if (mt >= tile_start[E]) return -1;
-  int lo = 0, hi = E - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tile_start[mid] <= mt) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
 }  // namespace moe
