@@ -596,7 +596,11 @@ struct DownDgradJobs {
     return true;
   }
   // staged drain: one slice per call; unit (row, 8 columns) of dA, whose G
-  // and U were loaded by the previous call (or the setup)
+  // and U were loaded by the previous call (or the setup).  With the adapter
+  // segment the stream has no registers to spare for that: G and U are then
+  // loaded in the call itself (its wait drains the loads in flight, which
+  // costs less than the spills the prefetch causes there).
+  static constexpr bool kPrefetch = !kLora;
   using Units = RowUnits<C, C::BN>;
   static constexpr bool kStaged = true;
   static constexpr int kDrainCalls = Units::kSlices;
@@ -620,11 +624,12 @@ struct DownDgradJobs {
   __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
     d.base = static_cast<int64_t>(j.m0) * F + j.n0;
     d.rows = j.m_lim;
-    prefetch(d, 0);
+    if constexpr (kPrefetch) prefetch(d, 0);
   }
   __device__ __forceinline__ void drain(Drain& d, const char* stg, int sl) const {
     const int s = sl < Units::kSlices ? sl : Units::kSlices - 1;
     const int r = Units::row(s), c = Units::chunk();
+    if constexpr (!kPrefetch) prefetch(d, sl);
     float da[8], gv[8], uv[8], dgv[8], duv[8];
     unpack8(*reinterpret_cast<const uint4*>(stg + Staged<C>::off(r, c)), da);
     unpack8(d.gw, gv);
@@ -637,7 +642,7 @@ struct DownDgradJobs {
     }
     buf_store16(rows_rsrc(dg_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(dgv));
     buf_store16(rows_rsrc(du_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(duv));
-    prefetch(d, sl + 1);
+    if constexpr (kPrefetch) prefetch(d, sl + 1);
   }
 };
 
