@@ -264,6 +264,9 @@ def main():
     ap.add_argument("--no-forward-only", action="store_true",
                     help="skip the forward-only (moe_infer), expert-LoRA and EP-share timings")
     ap.add_argument("--lora-rank", type=int, default=16, help="rank of the expert-LoRA timing")
+    ap.add_argument("--no-ep-share", action="store_true",
+                    help="skip the EP-share timing (its expert products have another shape, so a kernel "
+                         "trace of the block leaves it out)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one torch copy of MIB MiB before the steps (counter calibration)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -369,7 +372,7 @@ def main():
                                                                      args.warmup)
     lora = None if args.no_forward_only else lora_step(moe, t, tm, T, H, E, F, k, Tv, args.lora_rank,
                                                        args.steps, args.warmup)
-    ep = None if args.no_forward_only else ep_share_step(moe, args.steps, args.warmup)
+    ep = None if (args.no_forward_only or args.no_ep_share) else ep_share_step(moe, args.steps, args.warmup)
 
     gemm_flop = 18.0 * H * F * R
     router_flop = 6.0 * H * E * Tv
