@@ -53,7 +53,7 @@ def kernel_work(name, T, Tv, H, E, F, k, R):
         "dwr_partial": ("flop", 2.0 * Tv * H * E),
         "permute_rows": ("byte", float(Tv * H * b + R * H * b)),
         "combine": ("byte", float(R * H * b + Tv * H * b)),
-        "combine_bwd": ("byte", float(Tv * H * b + 2 * R * H * b)),
+        "combine_bwd": ("byte", float(Tv * H * b + R * H * b)),
         "router_dx": ("byte", float(R * H * b + Tv * H * b)),
     }.get(name, ("none", 0.0))
 

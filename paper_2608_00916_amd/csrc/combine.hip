@@ -1,5 +1,5 @@
-// Weighted combine of the expert outputs and its backward (which also forms
-// the router-logit gradient dz).  One wave per token; rows move as 16-byte
+// Weighted combine of the expert outputs, its backward, and the router-logit
+// gradient dz.  One wave per token; rows move as 16-byte
 // vectors (8 bf16 per lane), sums are fp32 in slot order.
 #include "launch.hpp"
 #include "trace.hpp"
@@ -60,11 +60,47 @@ __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, c
   }
 }
 
-// Per token t with rows r_j:
-//   dO[r_j]   = g_j dY[t]                                   (bf16)
+// dO[r_j] = g_j dY[t] for every routed slot of token t (bf16).
+template <int KT>
+__global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ dy, const float* __restrict__ gates,
+                                                     const int32_t* __restrict__ row_of, int T, int H, int k,
+                                                     bf16_t* __restrict__ d_o) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  int rows[KT];
+  float g[KT];
+#pragma unroll
+  for (int j = 0; j < KT; ++j) {
+    rows[j] = j < k ? row_of[static_cast<int64_t>(t) * k + j] : -1;
+    g[j] = j < k ? gates[static_cast<int64_t>(t) * k + j] : 0.0f;
+  }
+  if (rows[0] < 0) return;  // a masked token has no rows
+  const bf16_t* dyr = dy + static_cast<int64_t>(t) * H;
+  for (int c = lane * 8; c < H; c += kWave * 8) {
+    float fy[8];
+    unpack8(*reinterpret_cast<const uint4*>(dyr + c), fy);
+#pragma unroll
+    for (int j = 0; j < KT; ++j) {
+      if (rows[j] < 0) continue;
+      float out[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) out[i] = g[j] * fy[i];
+      *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(rows[j]) * H + c) = pack8(out);
+    }
+  }
+}
+
+// Per token t with rows r_j (one wave per token, lane j holds slot j):
 //   dg_j      = <dY[t], O[r_j]>                              (fp32)
 //   dz_j      = g_j (dg_j - sum_j' g_j' dg_j')               (fp32, per slot)
 //   dz[t, :]  = dz_j at e = idx_j, else 0                    (bf16, all E)
+// dg_j comes from the down product's backward instead of a second pass over
+// O: with dA = dO W_down^T and dO[r_j] = g_j dY[t], <dA[r_j], A[r_j]> =
+// <dO[r_j], A[r_j] W_down> = g_j <dY[t], O[r_j]>.  The down product's dgrad
+// writes that inner product per row and column block (part[r][p], p <
+// nparts), so dg_j = sum_p part[r_j][p] / g_j, and 0 where g_j = 0 (dz_j is 0
+// there either way).
 // With the router losses (RouterLossGrad.on) dz[t, :] also takes, for a
 // valid token, their gradient with the routing fractions f held constant:
 //   aux_coef E / T_v  p_e (f_e - sum_e' f_e' p_e') + z_coef 2 / T_v  lse p_e,
@@ -80,59 +116,29 @@ struct RouterLossGrad {
 constexpr int kMaxPerLane = MOE_MAX_EXPERTS / kWave;
 
 template <int KT, bool kAux>
-__device__ __forceinline__ void combine_bwd_body(const bf16_t* __restrict__ dy,
-                                                     const bf16_t* __restrict__ o,
-                                                     const float* __restrict__ gates,
-                                                     const int32_t* __restrict__ topk_idx,
-                                                     const int32_t* __restrict__ row_of, int T, int H,
-                                                     int E, int k, bf16_t* __restrict__ d_o,
-                                                     float* __restrict__ dg_out, float* __restrict__ dz_slot,
-                                                     bf16_t* __restrict__ dz, RouterLossGrad rl) {
+__global__ __launch_bounds__(256) void k_gate_bwd(const float* __restrict__ part, int nparts,
+                                                  const float* __restrict__ gates,
+                                                  const int32_t* __restrict__ topk_idx,
+                                                  const int32_t* __restrict__ row_of, int T, int E, int k,
+                                                  float* __restrict__ dg_out, float* __restrict__ dz_slot,
+                                                  bf16_t* __restrict__ dz, RouterLossGrad rl) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  int rows[KT];
-  float g[KT], part[KT];
-#pragma unroll
-  for (int j = 0; j < KT; ++j) {
-    rows[j] = j < k ? row_of[static_cast<int64_t>(t) * k + j] : -1;
-    g[j] = j < k ? gates[static_cast<int64_t>(t) * k + j] : 0.0f;
-    part[j] = 0.0f;
-  }
-  const bf16_t* dyr = dy + static_cast<int64_t>(t) * H;
-  for (int c = lane * 8; c < H; c += kWave * 8) {
-    const uint4 wy = *reinterpret_cast<const uint4*>(dyr + c);
-    uint4 v[KT];
-#pragma unroll
-    for (int j = 0; j < KT; ++j)
-      v[j] = rows[j] >= 0 ? *reinterpret_cast<const uint4*>(o + static_cast<int64_t>(rows[j]) * H + c)
-                          : make_uint4(0, 0, 0, 0);
-    float fy[8];
-    unpack8(wy, fy);
-#pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      if (rows[j] < 0) continue;
-      float fo[8], out[8];
-      unpack8(v[j], fo);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        part[j] += fy[i] * fo[i];
-        out[i] = g[j] * fy[i];
-      }
-      *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(rows[j]) * H + c) = pack8(out);
+  float my_g = 0.0f, my_dg = 0.0f;
+  int my_e = -1;
+  if (lane < k) {
+    const int64_t p = static_cast<int64_t>(t) * k + lane;
+    my_g = gates[p];
+    my_e = topk_idx[p];
+    const int r = row_of[p];
+    if (r >= 0) {
+      float sum = 0.0f;
+      for (int q = 0; q < nparts; ++q) sum += part[static_cast<int64_t>(r) * nparts + q];
+      my_dg = my_g != 0.0f ? sum / my_g : 0.0f;
     }
   }
-  float my_dg = 0.0f;  // lane j keeps dg_j
-#pragma unroll
-  for (int j = 0; j < KT; ++j) {
-    const float d = wave_sum(part[j]);
-    if (lane == j) my_dg = d;
-  }
-  float my_g = 0.0f;
-#pragma unroll
-  for (int j = 0; j < KT; ++j)
-    if (lane == j) my_g = g[j];
-  const int my_e = lane < k ? topk_idx[static_cast<int64_t>(t) * k + lane] : -1;
+  const bool valid = row_of[static_cast<int64_t>(t) * k] >= 0;  // slot 0 is routed
   const float inner = wave_sum(my_g * my_dg);
   const float my_dz = my_g * (my_dg - inner);
   if (lane < k) {
@@ -143,7 +149,7 @@ __device__ __forceinline__ void combine_bwd_body(const bf16_t* __restrict__ dy,
 #pragma unroll
   for (int m = 0; m < kMaxPerLane; ++m) extra[m] = 0.0f;
   if constexpr (kAux) {
-    if (rows[0] >= 0) {  // a valid token (slot 0 is routed)
+    if (valid) {
       const float* zr = rl.logits + static_cast<int64_t>(t) * E;
       const int R = rl.offsets[E];
       const float tv = static_cast<float>(R / k);
@@ -187,26 +193,11 @@ __device__ __forceinline__ void combine_bwd_body(const bf16_t* __restrict__ dy,
     for (int j = 0; j < KT; ++j) {
       const int ej = __shfl(my_e, j, kWave);
       const float dzj = __shfl(my_dz, j, kWave);
-      if (ej == e) v = dzj;
+      if (j < k && ej == e) v = dzj;
     }
     if (e < E) dzr[e] = f2bf(v + extra[m]);
   }
 }
-
-#define MOE_COMBINE_BWD_ALIAS(NAME, AUX)                                                                     \
-  template <int KT>                                                                                          \
-  __global__ __launch_bounds__(256) void NAME(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ o,   \
-                                              const float* __restrict__ gates,                               \
-                                              const int32_t* __restrict__ topk_idx,                          \
-                                              const int32_t* __restrict__ row_of, int T, int H, int E, int k, \
-                                              bf16_t* __restrict__ d_o, float* __restrict__ dg,              \
-                                              float* __restrict__ dz_slot, bf16_t* __restrict__ dz,          \
-                                              RouterLossGrad rl) {                                           \
-    combine_bwd_body<KT, AUX>(dy, o, gates, topk_idx, row_of, T, H, E, k, d_o, dg, dz_slot, dz, rl);        \
-  }
-MOE_COMBINE_BWD_ALIAS(k_combine_bwd_noaux, false)
-MOE_COMBINE_BWD_ALIAS(k_combine_bwd_aux, true)
-#undef MOE_COMBINE_BWD_ALIAS
 
 }  // namespace
 
@@ -219,6 +210,15 @@ MOE_COMBINE_BWD_ALIAS(k_combine_bwd_aux, true)
     else if ((k) <= 16) hipLaunchKernelGGL(KERNEL<16>, grid, dim3(256), 0, s, __VA_ARGS__); \
     else hipLaunchKernelGGL(KERNEL<32>, grid, dim3(256), 0, s, __VA_ARGS__);               \
   } while (0)
+#define MOE_SLOT_DISPATCH2(KERNEL, B, k, grid, s, ...)                                               \
+  do {                                                                                                \
+    if ((k) <= 1) hipLaunchKernelGGL((KERNEL<1, B>), grid, dim3(256), 0, s, __VA_ARGS__);             \
+    else if ((k) <= 2) hipLaunchKernelGGL((KERNEL<2, B>), grid, dim3(256), 0, s, __VA_ARGS__);        \
+    else if ((k) <= 4) hipLaunchKernelGGL((KERNEL<4, B>), grid, dim3(256), 0, s, __VA_ARGS__);        \
+    else if ((k) <= 8) hipLaunchKernelGGL((KERNEL<8, B>), grid, dim3(256), 0, s, __VA_ARGS__);        \
+    else if ((k) <= 16) hipLaunchKernelGGL((KERNEL<16, B>), grid, dim3(256), 0, s, __VA_ARGS__);      \
+    else hipLaunchKernelGGL((KERNEL<32, B>), grid, dim3(256), 0, s, __VA_ARGS__);                     \
+  } while (0)
 
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s) {
@@ -229,11 +229,19 @@ hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* ro
   return hipGetLastError();
 }
 
-hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
-                              const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz,
-                              const float* logits, const int32_t* counts, const int32_t* offsets,
-                              float aux_coef, float z_coef, hipStream_t s) {
+hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_t* row_of, int T, int H, int k,
+                              bf16_t* d_o, hipStream_t s) {
+  {
+    TraceScope trace_scope(K_COMBINE_BWD, s);
+    MOE_SLOT_DISPATCH(k_combine_bwd, k, dim3(cdiv(T, 4)), s, dy, gates, row_of, T, H, k, d_o);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_bwd(const float* part, int nparts, const float* gates, const int32_t* topk_idx,
+                           const int32_t* row_of, int T, int E, int k, float* dg, float* dz_slot, bf16_t* dz,
+                           const float* logits, const int32_t* counts, const int32_t* offsets, float aux_coef,
+                           float z_coef, hipStream_t s) {
   RouterLossGrad rl;
   const bool aux = aux_coef != 0.0f || z_coef != 0.0f;
   if (aux) {
@@ -244,13 +252,13 @@ hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* ga
     rl.z_coef = z_coef;
   }
   {
-    TraceScope trace_scope(K_COMBINE_BWD, s);
+    TraceScope trace_scope(K_GATE_BWD, s);
     if (aux)
-      MOE_SLOT_DISPATCH(k_combine_bwd_aux, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k, d_o,
-                        dg, dz_slot, dz, rl);
+      MOE_SLOT_DISPATCH2(k_gate_bwd, true, k, dim3(cdiv(T, 4)), s, part, nparts, gates, topk_idx, row_of, T, E, k, dg,
+                         dz_slot, dz, rl);
     else
-      MOE_SLOT_DISPATCH(k_combine_bwd_noaux, k, dim3(cdiv(T, 4)), s, dy, o, gates, topk_idx, row_of, T, H, E, k,
-                        d_o, dg, dz_slot, dz, rl);
+      MOE_SLOT_DISPATCH2(k_gate_bwd, false, k, dim3(cdiv(T, 4)), s, part, nparts, gates, topk_idx, row_of, T, E, k,
+                         dg, dz_slot, dz, rl);
   }
   return hipGetLastError();
 }

@@ -562,6 +562,26 @@ struct GateUpFwdJobs {
 // dG and dU, and by no one else.  With kLora a second segment Q2 a2[e]^T
 // (Q2 = scale dO b2^T, [rows][r]; a2 [E][F][r]: K-contiguous rows of the B
 // tile).  B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
+// Sum over aligned groups of N = 16 or 32 lanes with DPP moves (no LDS round
+// trips), in a fixed order: pairs, quads, eights, sixteens, and for N = 32
+// the two 16-lane rows.  The group total is in every lane of a 16-lane group,
+// and for N = 32 in the upper 16 lanes of the group.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), kCtrl, kRowMask, 0xf,
+                                                               false));
+}
+template <int N>
+__device__ __forceinline__ float row_sum_dpp(float v) {
+  static_assert(N == 16 || N == 32, "16- or 32-lane groups");
+  v += dpp_f<0xB1, 0xf>(v);   // quad_perm [1, 0, 3, 2]: lane ^ 1
+  v += dpp_f<0x4E, 0xf>(v);   // quad_perm [2, 3, 0, 1]: lane ^ 2
+  v += dpp_f<0x141, 0xf>(v);  // row_half_mirror: the other quad of each 8 lanes
+  v += dpp_f<0x140, 0xf>(v);  // row_mirror: the other 8 of each 16 lanes
+  if constexpr (N == 32) v += dpp_f<0x142, 0xa>(v);  // row_bcast15 into rows 1 and 3 (rows 0 and 2 add 0)
+  return v;
+}
+
 template <class C_, bool kLora>
 struct DownDgradJobs {
   using C = C_;
@@ -572,6 +592,7 @@ struct DownDgradJobs {
   int E, H, F;
   bf16_t *dg_out, *du_out;
   LoraSeg lo;
+  float* part;  // [rows][F / BN]: <dA, A> per row and column block, or null
   __device__ bool get(int i, Job<C>& j) const {
     MTile t;
     int seg;
@@ -599,18 +620,23 @@ struct DownDgradJobs {
   // and U were loaded by the previous call (or the setup).  With the adapter
   // segment the stream has no registers to spare for that: G and U are then
   // loaded in the call itself (its wait drains the loads in flight, which
-  // costs less than the spills the prefetch causes there).
+  // costs less than the spills the prefetch causes there).  With `part` the
+  // call also sums dA A = dU U over each of its rows' BN columns (fp32, the
+  // A = silu(G) U of the G and U it holds; a fixed DPP tree over the lanes of
+  // a row) for the gate gradient.
   static constexpr bool kPrefetch = !kLora;
   using Units = RowUnits<C, C::BN>;
   static constexpr bool kStaged = true;
   static constexpr int kDrainCalls = Units::kSlices;
   struct Drain {
-    int64_t base;  // element offset of the tile's (0, 0) in G, U, dG and dU
+    int64_t base;   // element offset of the tile's (0, 0) in G, U, dG and dU
+    int64_t pbase;  // element offset of the tile's first row and column block in part
     int rows;
     uint4 gw, uw;  // G and U of the next call's unit
   };
   __device__ __forceinline__ void drain_reset(Drain& d) const {
     d.base = 0;
+    d.pbase = 0;
     d.rows = 0;
     d.gw = d.uw = make_uint4(0, 0, 0, 0);
   }
@@ -623,6 +649,7 @@ struct DownDgradJobs {
   }
   __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
     d.base = static_cast<int64_t>(j.m0) * F + j.n0;
+    d.pbase = static_cast<int64_t>(j.m0) * (F / C::BN) + j.n0 / C::BN;
     d.rows = j.m_lim;
     if constexpr (kPrefetch) prefetch(d, 0);
   }
@@ -634,14 +661,26 @@ struct DownDgradJobs {
     unpack8(*reinterpret_cast<const uint4*>(stg + Staged<C>::off(r, c)), da);
     unpack8(d.gw, gv);
     unpack8(d.uw, uv);
+    float dot = 0.0f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float sg = sigmoid_f(gv[i]);
       dgv[i] = da[i] * uv[i] * sg * (1.0f + gv[i] * (1.0f - sg));
       duv[i] = da[i] * gv[i] * sg;
+      dot += duv[i] * uv[i];  // dA silu(G) U = dA A
     }
     buf_store16(rows_rsrc(dg_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(dgv));
     buf_store16(rows_rsrc(du_out + d.base, d.rows, F * 2, C::BN * 2), unit_off(sl), pack8(duv));
+    // unconditional (a null `part` gets an empty resource), so the stream's
+    // vector-memory count per call is fixed and its waits stay exact
+    dot = row_sum_dpp<Units::kCpr>(dot);
+    const int np = F / C::BN;
+    const bool writer = c == (Units::kCpr == 32 ? 16 : 0);
+    const uint32_t poff = (writer && sl < Units::kSlices) ? static_cast<uint32_t>(r * np * 4) : kOob;
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, dot),
+                                          rows_rsrc(part != nullptr ? part + d.pbase : nullptr,
+                                                    part != nullptr ? d.rows : 0, np * 4, 4),
+                                          static_cast<int>(poff), 0, 0);
     if constexpr (kPrefetch) prefetch(d, sl + 1);
   }
 };
@@ -690,6 +729,9 @@ int persistent_grid(Kernel kernel, int threads, int64_t max_tiles) {
 // Upper bound of the number of 128-row tiles over all experts.
 int max_row_tiles(int rows_cap, int E) { return cdiv(rows_cap, kRowTile) + E; }
 
+// The dgrad of the down product runs 256-column tiles when F allows, else 128.
+int dgate_parts(int F) { return F % 256 == 0 ? F / 256 : F / 128; }
+
 namespace {
 
 // Tile shapes: 128 rows x 256 columns over 8 waves (2 x 4, 64 x 64 each, two
@@ -735,11 +777,11 @@ void down_dgrad(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du, 
   const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.F / C::BN);
   if (lo.rank > 0)
     run_stream<true, true>(DownDgradJobs<C, true>{d_o, a.w_down, a.g, a.u, a.tile_start, a.tile_desc, a.E, a.H, a.F,
-                                                  dg, du, lo},
+                                                  dg, du, lo, a.dgate_part},
                            tiles, K_DOWN_DGRAD, s);
   else
     run_stream<true, true>(DownDgradJobs<C, false>{d_o, a.w_down, a.g, a.u, a.tile_start, a.tile_desc, a.E, a.H, a.F,
-                                                   dg, du, lo},
+                                                   dg, du, lo, a.dgate_part},
                            tiles, K_DOWN_DGRAD, s);
 }
 

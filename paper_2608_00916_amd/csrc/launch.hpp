@@ -45,10 +45,16 @@ struct ExpertArgs {
   // of xp (then the unpermuted tokens, xp_bytes < 2^31 bytes in all).
   const int32_t* xp_rows = nullptr;
   int64_t xp_bytes = 0;
+  // Down product's dgrad only: when non-null, it also writes
+  // dgate_part[r][p] = <dA[r], A[r]> over its column block p
+  // (dgate_parts(F) blocks; A = silu(G) U in fp32).
+  float* dgate_part = nullptr;
   LoraArgs lora;
 };
 
 int max_row_tiles(int rows_cap, int E);
+// Column blocks of the down product's dgrad (the dgate_part row length).
+int dgate_parts(int F);
 
 // G, U, A from Xp (gate/up products + SwiGLU); G and U are skipped when
 // a.g is null, A when a.act is.  `recompute` only names the launch in traces
@@ -113,15 +119,19 @@ hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, in
 // y[t] = sum_j gates[t,j] o[row_of[t,j]] (0 for masked tokens).
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s);
-// dO[row_of[t,j]] = g dY[t]; dg = <dY[t], O[row]>; dz per slot (fp32 [T,k])
-// and dense over E (bf16 [T,E]).  With a non-zero router-loss coefficient the
-// dense dz also takes the router losses' gradient (from the fp32 logits, the
-// counts and offsets); dz per slot stays the gates' part.
-hipError_t launch_combine_bwd(const bf16_t* dy, const bf16_t* o, const float* gates,
-                              const int32_t* topk_idx, const int32_t* row_of, int T, int H, int E,
-                              int k, bf16_t* d_o, float* dg, float* dz_slot, bf16_t* dz,
-                              const float* logits, const int32_t* counts, const int32_t* offsets,
-                              float aux_coef, float z_coef, hipStream_t s);
+// dO[row_of[t,j]] = g dY[t] for every routed slot.
+hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_t* row_of, int T, int H, int k,
+                              bf16_t* d_o, hipStream_t s);
+// After the down product's dgrad (which leaves part[r][0..nparts), the inner
+// products <dA[r], A[r]> per column block): dg = <dY[t], O[row]> = sum / g,
+// dz per slot (fp32 [T,k]) and dense over E (bf16 [T,E]).  With a non-zero
+// router-loss coefficient the dense dz also takes the router losses' gradient
+// (from the fp32 logits, the counts and offsets); dz per slot stays the gates'
+// part.
+hipError_t launch_gate_bwd(const float* part, int nparts, const float* gates, const int32_t* topk_idx,
+                           const int32_t* row_of, int T, int E, int k, float* dg, float* dz_slot, bf16_t* dz,
+                           const float* logits, const int32_t* counts, const int32_t* offsets, float aux_coef,
+                           float z_coef, hipStream_t s);
 
 // ---- router backward (router_bwd.hip)
 int dwr_splits(int T);

@@ -153,6 +153,7 @@ struct BwdWs {
   bf16_t* d_o;  // also dXp once dO is dead
   bf16_t *dg, *du, *dz, *w_rt;
   float *dgate, *dz_slot, *dwr_part;
+  float* dgate_part;  // <dA, A> per row and column block of the down product's dgrad
   float* dense;  // dz W_r^T (fp32 [T,H]) when the router losses are on
   size_t bytes;
 };
@@ -167,6 +168,7 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
   w.dz = c.take<bf16_t>(T * E);
   w.dgate = c.take<float>(T * k);
   w.dz_slot = c.take<float>(T * k);
+  w.dgate_part = c.take<float>(R * static_cast<size_t>(dgate_parts(d->F)));
   w.w_rt = c.take<bf16_t>(E * H);
   w.dwr_part = c.take<float>(static_cast<size_t>(dwr_splits(d->T)) * H * E);
   w.dense = router_losses(d) ? c.take<float>(T * H) : nullptr;
@@ -445,16 +447,19 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   const Saved sv = saved_layout(d, const_cast<void*>(saved));
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bool f32 = d->flags & MOE_F_DW_FP32;
-  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
-                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, sv.logits, sv.counts,
-                                    sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.gates, sv.row_of, T, H, k, w.d_o, s);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
+  a.dgate_part = w.dgate_part;
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // dXp reuses dO's memory: the down products that read dO are queued first.
   e = launch_experts_bwd_data(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_down, f32, s);
   if (e != hipSuccess) return hip_status(e, "experts bwd");
+  // gate gradients and dz from the down dgrad's <dA, A> sums
+  e = launch_gate_bwd(w.dgate_part, dgate_parts(F), sv.gates, sv.topk_idx, sv.row_of, T, E, k, w.dgate, w.dz_slot,
+                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+  if (e != hipSuccess) return hip_status(e, "gate bwd");
   // dX right after dXp, while much of dXp is still in the last-level cache.
   e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
                        w.w_rt, static_cast<bf16_t*>(dx), w.dense != nullptr ? w.dz : nullptr, w.dense, s);
@@ -498,19 +503,21 @@ int moe_lora_bwd(const moe_dims* d, const void* x, const void* w_r, const void* 
   const Saved sv = saved_layout(d, const_cast<void*>(saved));
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k, r = lora->rank;
   const bool f32 = d->flags & MOE_F_DW_FP32;
-  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.o, sv.gates, sv.topk_idx, sv.row_of,
-                                    T, H, E, k, w.d_o, w.dgate, w.dz_slot, w.dz, sv.logits, sv.counts,
-                                    sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.gates, sv.row_of, T, H, k, w.d_o, s);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
   a.lora = lora_args(lora, lora_saved_layout(d, r, const_cast<void*>(saved)));
+  a.dgate_part = w.dgate_part;
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // Q2 = scale dO b2^T (b2 [E][r][H]: rows q of the B operand, K-contiguous)
   e = launch_lora_rows(a, w.d_o, nullptr, H, a.lora.b2, nullptr, static_cast<int64_t>(r) * H, H, true, lw.q2, s);
   if (e != hipSuccess) return hip_status(e, "LoRA Q2");
   e = launch_down_dgrad(a, w.d_o, w.dg, w.du, lw.q2, s);
   if (e != hipSuccess) return hip_status(e, "down dgrad");
+  e = launch_gate_bwd(w.dgate_part, dgate_parts(F), sv.gates, sv.topk_idx, sv.row_of, T, E, k, w.dgate, w.dz_slot,
+                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+  if (e != hipSuccess) return hip_status(e, "gate bwd");
   // d a2 = A^T Q2 ([E][F][r]); d b2 = P2^T dO, formed as (dO^T P2)^T ([E][r][H])
   e = launch_lora_wgrad(a, sv.a, F, F, lw.q2, false, da2, f32, s);
   if (e != hipSuccess) return hip_status(e, "LoRA d a2");

@@ -33,6 +33,7 @@ enum KernelId {
   K_ROUTER_DX_DENSE,
   K_LORA_ROWS,
   K_LORA_WGRAD,
+  K_GATE_BWD,
   K_NUM_KERNELS
 };
 
