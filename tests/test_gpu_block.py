@@ -130,6 +130,21 @@ def test_edge_shapes(case):
     compare(inp, gpu_run(inp), f, b)
 
 
+def test_underflowing_gates():
+    """Router logits far apart (W_r scaled up 1000x): many second gates are
+    exactly 0 in fp32.  The gate gradient then takes its g = 0 branch
+    (dg = 0, so dz = g (dg - sum g dg) stays 0, as the fp64 oracle's tiny g
+    makes it) instead of dividing by zero."""
+    inp = workloads.block_inputs(T=200, H=128, E=8, k=2, F=128, seed=41)
+    inp["w_r"] = workloads.bf16_bits((O.widen_bf16(inp["w_r"]) * 1000.0).astype(np.float32))
+    f, b = oracle_run(inp)
+    g = gpu_run(inp)
+    assert (g["gates"][:, 1] == 0).sum() >= 20, "the case needs gates that underflow"
+    for n in ("dx", "dw_r"):
+        assert np.all(np.isfinite(g[n]))
+    compare(inp, g, f, b)
+
+
 @pytest.mark.parametrize("frac", [0.3, 1.0])
 def test_masked_tokens(frac):
     inp = workloads.block_inputs(T=333, H=256, E=16, k=2, F=128, seed=31)
