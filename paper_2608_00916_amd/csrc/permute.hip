@@ -72,69 +72,71 @@ __device__ __forceinline__ void write_tiles(int e, int off, int n, int toff, int
   for (int i = 0; i * 128 < n; ++i) tile_desc[toff + i] = make_int2(off + i * 128, e | (min(128, n - i * 128) << 8));
 }
 
-// One workgroup: counts[e], offsets = exclusive scan (E+1), tile_start of
-// 128-row tiles (E+1) and the tile table, and chunk_base[c][e] = rows of
-// expert e in chunks before c.  The chunk counts pass through LDS in batches,
-// so each batch costs one round of parallel loads.
-constexpr int kScanBatch = 32;
-
-__global__ __launch_bounds__(256) void k_perm_scan(const int32_t* __restrict__ chunk_counts, int nchunks,
-                                                   int E, int32_t* __restrict__ chunk_base,
-                                                   int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
-                                                   int32_t* __restrict__ tile_start, int2* __restrict__ tile_desc) {
-  __shared__ int tmp[256];
-  __shared__ int cc[kScanBatch][MOE_MAX_EXPERTS];
-  const int e = threadIdx.x;
-  int running = 0;
-  for (int c0 = 0; c0 < nchunks; c0 += kScanBatch) {
-    const int nb = min(kScanBatch, nchunks - c0);
-    for (int i = threadIdx.x; i < nb * E; i += 256) cc[i / E][i % E] = chunk_counts[static_cast<int64_t>(c0) * E + i];
-    __syncthreads();
-    if (e < E)
-      for (int c = 0; c < nb; ++c) {
-        chunk_base[static_cast<int64_t>(c0 + c) * E + e] = running;
-        running += cc[c][e];
-      }
-    __syncthreads();
-  }
-  const int n = e < E ? running : 0;
-  const int off = block_exclusive_scan(n, tmp);
-  const int tiles = cdiv(n, 128);
-  const int toff = block_exclusive_scan(tiles, tmp);
-  if (e < E) {
-    counts[e] = n;
-    offsets[e] = off;
-    tile_start[e] = toff;
-    write_tiles(e, off, n, toff, tile_desc);
-  }
-  if (e == E - 1) {
-    offsets[E] = off + n;
-    tile_start[E] = toff + tiles;
-  }
-}
-
+// Per chunk c (one workgroup): from the chunk counts of every chunk, expert
+// e's rows in chunks before c and in all chunks (integer sums in chunk
+// order), the offsets (an exclusive scan over experts), then the chunk's
+// pairs go to row offsets[e] + (rows of e in earlier chunks) + (rank inside
+// the chunk: a popcount of the lower tokens' bits).  Workgroup 0 also writes
+// counts, offsets[E+1], tile_start[E+1] and the tile table.
 __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restrict__ topk_idx, int T, int E,
-                                                         int k, const int32_t* __restrict__ chunk_base,
-                                                         const int32_t* __restrict__ offsets,
+                                                         int k, const int32_t* __restrict__ chunk_counts,
+                                                         int nchunks, int32_t* __restrict__ counts,
+                                                         int32_t* __restrict__ offsets,
+                                                         int32_t* __restrict__ tile_start,
+                                                         int2* __restrict__ tile_desc,
                                                          int32_t* __restrict__ row_token,
                                                          int32_t* __restrict__ row_of) {
   __shared__ unsigned long long bits[MOE_MAX_EXPERTS][kWords];
+  __shared__ int tmp[256];
+  __shared__ int base[MOE_MAX_EXPERTS];  // offsets[e] + rows of e in earlier chunks
   const int chunk = blockIdx.x;
-  build_bits(bits, topk_idx, T, E, k, chunk);
+  const int e = threadIdx.x;
+  int before = 0, total = 0;
+  if (e < E) {
+    constexpr int kBatch = 16;  // independent loads in flight per thread
+    for (int c0 = 0; c0 < nchunks; c0 += kBatch) {
+      int n[kBatch];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        n[i] = c0 + i < nchunks ? chunk_counts[static_cast<int64_t>(c0 + i) * E + e] : 0;
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        before += c0 + i < chunk ? n[i] : 0;
+        total += n[i];
+      }
+    }
+  }
+  const int off = block_exclusive_scan(e < E ? total : 0, tmp);
+  if (e < E) base[e] = off + before;
+  if (chunk == 0) {
+    const int tiles = cdiv(total, 128);
+    const int toff = block_exclusive_scan(e < E ? tiles : 0, tmp);
+    if (e < E) {
+      counts[e] = total;
+      offsets[e] = off;
+      tile_start[e] = toff;
+      write_tiles(e, off, total, toff, tile_desc);
+    }
+    if (e == E - 1) {
+      offsets[E] = off + total;
+      tile_start[E] = toff + tiles;
+    }
+  }
+  build_bits(bits, topk_idx, T, E, k, chunk);  // its barriers also publish base[]
   const int t = chunk * kChunk + threadIdx.x;
   if (t >= T) return;
   const int w = threadIdx.x >> 6;
   const unsigned long long below = (1ull << (threadIdx.x & 63)) - 1ull;
   for (int j = 0; j < k; ++j) {
     const int64_t p = static_cast<int64_t>(t) * k + j;
-    const int e = topk_idx[p];
-    if (e < 0) {
+    const int ej = topk_idx[p];
+    if (ej < 0) {
       row_of[p] = -1;
       continue;
     }
-    int rank = __popcll(bits[e][w] & below);
-    for (int ww = 0; ww < w; ++ww) rank += __popcll(bits[e][ww]);
-    const int r = offsets[e] + chunk_base[static_cast<int64_t>(chunk) * E + e] + rank;
+    int rank = __popcll(bits[ej][w] & below);
+    for (int ww = 0; ww < w; ++ww) rank += __popcll(bits[ej][ww]);
+    const int r = base[ej] + rank;
     row_token[r] = t;
     row_of[p] = r;
   }
@@ -206,28 +208,22 @@ __global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __re
 
 }  // namespace
 
-int64_t permute_ws_ints(int T, int E) { return 2 * static_cast<int64_t>(cdiv(T, kChunk)) * E; }
+int64_t permute_ws_ints(int T, int E) { return static_cast<int64_t>(cdiv(T, kChunk)) * E; }
 
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
                           int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
   const int nchunks = cdiv(T, kChunk);
   int32_t* chunk_counts = ws;
-  int32_t* chunk_base = ws + static_cast<int64_t>(nchunks) * E;
   {
     TraceScope trace_scope(K_PERM_HIST, s);
     hipLaunchKernelGGL(k_perm_hist, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts,
                        row_token);
   }
   {
-    TraceScope trace_scope(K_PERM_SCAN, s);
-    hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(256), 0, s, chunk_counts, nchunks, E, chunk_base, counts,
-                       offsets, tile_start, tile_desc);
-  }
-  {
     TraceScope trace_scope(K_PERM_SCATTER, s);
-    hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_base,
-                       offsets, row_token, row_of);
+    hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts, nchunks,
+                       counts, offsets, tile_start, tile_desc, row_token, row_of);
   }
   if (xp == nullptr) return hipGetLastError();
   // a few waves per CU suffice: each token's row is read once and written k times

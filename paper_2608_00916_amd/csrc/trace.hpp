@@ -12,7 +12,6 @@ enum KernelId {
   K_ROUTER_LOGITS,
   K_TOPK,
   K_PERM_HIST,
-  K_PERM_SCAN,
   K_PERM_SCATTER,
   K_PERMUTE_ROWS,
   K_GATEUP_FWD,
