@@ -91,11 +91,13 @@ hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, co
 
 // ---- routing (router.hip)
 // logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
-// With aux_ws (router_loss_ws_floats(T, E) floats) also the per-workgroup
-// partial sums of the router losses.
+// `part` (router_part_floats(T, E) floats) holds the partial sums of the
+// K-split logits product.  With aux_ws (router_loss_ws_floats(T, E) floats)
+// also the per-workgroup partial sums of the router losses.
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
-                             int E, int k, float* logits, int32_t* topk_idx, float* gates, float* aux_ws,
-                             hipStream_t s);
+                             int E, int k, float* logits, float* part, int32_t* topk_idx, float* gates,
+                             float* aux_ws, hipStream_t s);
+int64_t router_part_floats(int T, int E);
 int64_t router_loss_ws_floats(int T, int E);
 // out[0..1] = {L_aux, L_z} from those partial sums and the routing counts.
 hipError_t launch_router_loss(const float* aux_ws, int T, int E, int k, const int32_t* counts,

@@ -133,6 +133,7 @@ Saved saved_layout(const moe_dims* d, void* base) {
 // losses' partial sums when they are on
 struct FwdWs {
   int32_t* perm;
+  float* router_part;
   float* loss;
   size_t bytes;
 };
@@ -141,6 +142,7 @@ FwdWs fwd_layout(const moe_dims* d, void* base) {
   Carve c(base);
   FwdWs w;
   w.perm = c.take<int32_t>(static_cast<size_t>(permute_ws_ints(d->T, d->E)));
+  w.router_part = c.take<float>(static_cast<size_t>(router_part_floats(d->T, d->E)));
   w.loss = router_losses(d) ? c.take<float>(static_cast<size_t>(router_loss_ws_floats(d->T, d->E))) : nullptr;
   w.bytes = c.off;
   return w;
@@ -180,6 +182,7 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
 // rows only when x is too large to be read through the permutation, A and O.
 struct InferWs {
   float* logits;
+  float* router_part;
   int32_t *topk_idx, *counts, *offsets, *tile_start, *row_token, *row_of, *perm;
   int2* tile_desc;
   float* gates;
@@ -198,6 +201,7 @@ InferWs infer_layout(const moe_dims* d, void* base) {
   Carve c(base);
   InferWs w;
   w.logits = c.take<float>(T * E);
+  w.router_part = c.take<float>(static_cast<size_t>(router_part_floats(d->T, d->E)));
   w.topk_idx = c.take<int32_t>(T * k);
   w.gates = c.take<float>(T * k);
   w.counts = c.take<int32_t>(E);
@@ -353,7 +357,7 @@ int block_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, sv.logits, sv.topk_idx, sv.gates, fw.loss, s);
+                                   E, k, sv.logits, fw.router_part, sv.topk_idx, sv.gates, fw.loss, s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
                      sv.row_of, sv.xp, fw.perm, s);
@@ -561,7 +565,7 @@ int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, w.logits, w.topk_idx, w.gates, nullptr, s);
+                                   E, k, w.logits, w.router_part, w.topk_idx, w.gates, nullptr, s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.tile_desc, w.row_token, w.row_of,
                      w.xp, w.perm, s);

@@ -13,25 +13,39 @@ namespace {
 
 static_assert(MOE_MAX_EXPERTS <= 4 * kWave, "at most four experts per lane in the top-k");
 
-// Logits z = x W_r, fp32 [T][E]: one workgroup per 32 tokens and all E
-// experts (bf16 MFMA, fp32 accumulate, K = H), one 128-expert column tile at
-// a time, so T / 32 workgroups share the chip.
-using RouterTile = Tile<32, 128, 1, 1, 4>;
+// Logits z = x W_r, fp32 [T][E], split over K: workgroup (i, s) multiplies
+// tokens 128 i .. 128 i + 127 by W_r over the s-th of kRouterSplits
+// contiguous K ranges (whole 64-deep steps) and writes its partial sums,
+// split 0 into `logits` and split s > 0 into part[s - 1] ([T][E] each); the
+// top-k kernel adds them in split order.  All E experts per workgroup, one
+// 128-expert column tile at a time (bf16 MFMA, fp32 accumulate).  Every
+// workgroup streams its K range of W_r (512 KB in all at H = 2048, E = 128)
+// through LDS, so the token tile sets how often W_r crosses from L2: 128
+// tokens per tile and a 4-way K split keep the grid at T / 32 workgroups
+// while W_r is read T / 128 times instead of T / 32.
+using RouterTile = Tile<128, 128, 1, 2, 2>;
 constexpr int kRouterTokens = RouterTile::BM;
+constexpr int kRouterSplits = 4;
 
 __global__ __launch_bounds__(RouterTile::kThreads) void k_router_logits(const bf16_t* __restrict__ x,
                                                                         const bf16_t* __restrict__ w_r, int T,
-                                                                        int H, int E, float* __restrict__ logits) {
+                                                                        int H, int E, float* __restrict__ logits,
+                                                                        float* __restrict__ part) {
   using C = RouterTile;
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
   const int t0 = blockIdx.x * kRouterTokens;
   const int rows = min(kRouterTokens, T - t0);
+  const int split = blockIdx.y;
+  const int kper = cdiv(cdiv(H, kRouterSplits), BK) * BK;
+  const int k0 = min(H, split * kper);
+  const int kn = min(H, k0 + kper) - k0;  // 0 for an empty split: its partial sums are zeros
+  float* out = split == 0 ? logits : part + static_cast<int64_t>(split - 1) * T * E;
   const int lane = threadIdx.x & 63;
   for (int n0 = 0; n0 < E; n0 += C::BN) {
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
-    const bf16_t* bs[1] = {w_r + n0};  // B(k = h, n = e) = W_r[h][e]: E-contiguous
-    gemm_mainloop<C, true, false>(x + static_cast<int64_t>(t0) * H, H, rows, bs, E, E - n0, H, smem, acc);
+    const bf16_t* bs[1] = {w_r + static_cast<int64_t>(k0) * E + n0};  // B(k = h, n = e) = W_r[h][e]: E-contiguous
+    gemm_mainloop<C, true, false>(x + static_cast<int64_t>(t0) * H + k0, H, rows, bs, E, E - n0, kn, smem, acc);
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
       const int r = frag_row<C>(mi, lane);
@@ -41,8 +55,7 @@ __global__ __launch_bounds__(RouterTile::kThreads) void k_router_logits(const bf
         const int e = n0 + frag_col<C>(ni, lane);
         if (e < E) {  // E % 8 == 0, so e < E covers e..e+3
           const f32x4 v = acc[mi][ni];
-          *reinterpret_cast<float4*>(logits + static_cast<int64_t>(t0 + r) * E + e) =
-              make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(out + static_cast<int64_t>(t0 + r) * E + e) = make_float4(v[0], v[1], v[2], v[3]);
         }
       }
     }
@@ -143,23 +156,35 @@ __device__ __forceinline__ float topk_select(const float (&val)[PL], const uint3
 // (lse_t = log sum_e exp z[t,e]).  Many waves per SIMD hide the latency of
 // the wave-wide counts.
 template <int PL, bool kAux>
-__global__ __launch_bounds__(256) void k_topk(const float* __restrict__ logits, const uint8_t* __restrict__ mask,
-                                              int T, int E, int k, int32_t* __restrict__ topk_idx,
-                                              float* __restrict__ gates, float* __restrict__ aux_part) {
+__global__ __launch_bounds__(256) void k_topk(float* __restrict__ logits, const float* __restrict__ part,
+                                              const uint8_t* __restrict__ mask, int T, int E, int k,
+                                              int32_t* __restrict__ topk_idx, float* __restrict__ gates,
+                                              float* __restrict__ aux_part) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int t = blockIdx.x * 4 + wv;
   if (!kAux && t >= T) return;
   const bool on = t < T && (mask == nullptr || mask[t] != 0);
   float val[PL];
   uint32_t key[PL];
-  if (on) {
-    const float* z = logits + static_cast<int64_t>(t) * E;
+  if (t < T) {
+    // z = the K splits' partial sums added in split order, stored back as the logits
+    float* z = logits + static_cast<int64_t>(t) * E;
+    const int64_t plane = static_cast<int64_t>(T) * E;
 #pragma unroll
     for (int m = 0; m < PL; ++m) {
       const int e = lane + kWave * m;
-      val[m] = e < E ? z[e] : 0.0f;
-      key[m] = e < E ? order_key(val[m]) : 0u;
+      float v = 0.0f;
+      if (e < E) {
+        v = z[e];
+#pragma unroll
+        for (int sp = 0; sp < kRouterSplits - 1; ++sp) v += part[sp * plane + static_cast<int64_t>(t) * E + e];
+        z[e] = v;
+      }
+      val[m] = v;
+      key[m] = e < E ? order_key(v) : 0u;
     }
+  }
+  if (on) {
     topk_select<PL>(val, key, k, lane, topk_idx + static_cast<int64_t>(t) * k, gates + static_cast<int64_t>(t) * k);
   } else if (t < T && lane < k) {
     topk_idx[static_cast<int64_t>(t) * k + lane] = -1;
@@ -242,21 +267,22 @@ __global__ __launch_bounds__(256) void k_router_loss_final(const float* __restri
 }  // namespace
 
 int64_t router_loss_ws_floats(int T, int E) { return static_cast<int64_t>(cdiv(T, 4)) * (E + 1) + E + 1; }
+int64_t router_part_floats(int T, int E) { return static_cast<int64_t>(kRouterSplits - 1) * T * E; }
 
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
-                             int E, int k, float* logits, int32_t* topk_idx, float* gates, float* aux_ws,
-                             hipStream_t s) {
+                             int E, int k, float* logits, float* part, int32_t* topk_idx, float* gates,
+                             float* aux_ws, hipStream_t s) {
   {
     TraceScope trace_scope(K_ROUTER_LOGITS, s);
-    hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, kRouterTokens)), dim3(RouterTile::kThreads), 0, s, x, w_r,
-                       T, H, E, logits);
+    hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, kRouterTokens), kRouterSplits), dim3(RouterTile::kThreads), 0,
+                       s, x, w_r, T, H, E, logits, part);
   }
   {
     TraceScope trace_scope(K_TOPK, s);
     const dim3 grid(cdiv(T, 4)), block(256);
     // experts per lane: 1, 2 or 4 (E <= 256)
 #define MOE_TOPK(PL, AUX) \
-  hipLaunchKernelGGL((k_topk<PL, AUX>), grid, block, 0, s, logits, mask, T, E, k, topk_idx, gates, aux_ws)
+  hipLaunchKernelGGL((k_topk<PL, AUX>), grid, block, 0, s, logits, part, mask, T, E, k, topk_idx, gates, aux_ws)
     const bool aux = aux_ws != nullptr;
     if (E <= kWave) {
       if (aux) MOE_TOPK(1, true); else MOE_TOPK(1, false);
