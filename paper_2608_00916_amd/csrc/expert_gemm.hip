@@ -555,13 +555,6 @@ struct GateUpFwdJobs {
   }
 };
 
-// dA = dO W_down[e]^T (K = H, N = F) fused with the SwiGLU backward:
-// s = sigmoid(G); dG = dA U s (1 + G (1 - s)); dU = dA G s, with dA the
-// bf16 product.  dG and dU may overwrite G and U in place: each element of
-// G and U is read by the one thread that later writes the same element of
-// dG and dU, and by no one else.  With kLora a second segment Q2 a2[e]^T
-// (Q2 = scale dO b2^T, [rows][r]; a2 [E][F][r]: K-contiguous rows of the B
-// tile).  B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
 // Sum over aligned groups of N = 16 or 32 lanes with DPP moves (no LDS round
 // trips), in a fixed order: pairs, quads, eights, sixteens, and for N = 32
 // the two 16-lane rows.  The group total is in every lane of a 16-lane group,
@@ -582,6 +575,13 @@ __device__ __forceinline__ float row_sum_dpp(float v) {
   return v;
 }
 
+// dA = dO W_down[e]^T (K = H, N = F) fused with the SwiGLU backward:
+// s = sigmoid(G); dG = dA U s (1 + G (1 - s)); dU = dA G s, with dA the
+// bf16 product.  dG and dU may overwrite G and U in place: each element of
+// G and U is read by the one thread that later writes the same element of
+// dG and dU, and by no one else.  With kLora a second segment Q2 a2[e]^T
+// (Q2 = scale dO b2^T, [rows][r]; a2 [E][F][r]: K-contiguous rows of the B
+// tile).  B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
 template <class C_, bool kLora>
 struct DownDgradJobs {
   using C = C_;
