@@ -368,7 +368,7 @@ __device__ __forceinline__ void row_job_fill(Job<C>& j, const MTile& t, int n0, 
 // O = A W_down[e]  (K = F, N = H); with kLora a second segment P2 b2[e]
 // (P2 = scale A a2, [rows][r]; b2 [E][r][H], MN-contiguous like W_down).
 template <class C_, bool kLora>
-struct DownFwdJobs : StagedCopyOut<C_, DownFwdJobs<C_, kLora>> {
+struct DownFwdJobs : StagedCopyOut<C_, DownFwdJobs<C_, kLora>, /*kKeep=*/true> {  // O: the combine reads it next
   using C = C_;
   const bf16_t *act, *w_down;
   const int32_t* tile_start;
@@ -411,7 +411,7 @@ struct DownFwdJobs : StagedCopyOut<C_, DownFwdJobs<C_, kLora>> {
 // [rows][r]; a1 [E][H][r]: K-contiguous rows of the B tile).  B(k = f,
 // n = h) = W[e][h][f]: K-contiguous rows of W_gate / W_up.
 template <class C_, bool kLora>
-struct GateUpDgradJobs : StagedCopyOut<C_, GateUpDgradJobs<C_, kLora>> {
+struct GateUpDgradJobs : StagedCopyOut<C_, GateUpDgradJobs<C_, kLora>, /*kKeep=*/true> {  // dXp: the router dX reads it next
   using C = C_;
   const bf16_t *dg, *du, *w_gate, *w_up;
   const int32_t* tile_start;

@@ -461,8 +461,15 @@ constexpr int stream_lds() {
   return P::C::kLds + (staged_provider<P>::value ? Staged<typename P::C>::kBytes : 0);
 }
 
+// Output stores of the grouped products are non-temporal (streamed past the
+// caches, so that they do not evict the operands the next tiles reuse),
+// except where a memory-bound kernel reads the output straight back
+// (kKeep: it may then still find it in the last-level cache).
+template <bool kKeep = false>
 __device__ __forceinline__ void buf_store16(__amdgpu_buffer_rsrc_t r, uint32_t off, const uint4& v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), r, static_cast<int>(off), 0, 0);
+  constexpr int kNonTemporal = 2;  // the nt cache-policy bit of a buffer store
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), r, static_cast<int>(off), 0,
+                                         kKeep ? 0 : kNonTemporal);
 }
 
 // Buffer resource over `rows` rows of `width_bytes` at pitch ld_bytes:
@@ -476,8 +483,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void* base, in
 // Drain that copies the staged tile to NB destinations (element (0, 0) of
 // each BM x BNS block, pitch ld elements, `rows` valid rows; whole rows of BNS
 // columns are written).  A slice is one 16-byte chunk per thread: wave w
-// stores block w % NB, kRowsPerWave rows of it per slice.
-template <class C>
+// stores block w % NB, kRowsPerWave rows of it per slice.  kKeep: cached
+// stores (see buf_store16).
+template <class C, bool kKeep = false>
 struct StagedCopy {
   using SO = Staged<C>;
   static constexpr int kCpr = C::BNS * 2 / 16;  // chunks per block row
@@ -512,7 +520,7 @@ struct StagedCopy {
     const uint4 v = *reinterpret_cast<const uint4*>(stg + SO::off(row0, (wv % C::NB) * kCpr + cq) +
                                                     s * (kSliceRows * SO::kRowBytes));
     const uint32_t off = static_cast<uint32_t>(row0 + s * kSliceRows) * d.ld + cq * 16;
-    buf_store16(d.out, sl < kSlices ? off : kOob, v);
+    buf_store16<kKeep>(d.out, sl < kSlices ? off : kOob, v);
   }
   __device__ static __forceinline__ void call(const State& d, const char* stg, int p) {  // two slices
     slice(d, stg, 2 * p);
@@ -521,21 +529,23 @@ struct StagedCopy {
 };
 
 // Mixin for providers whose staged tiles are copied out unchanged; Derived
-// supplies stage_dst(job, dst, ld, rows).
-template <class C, class Derived>
+// supplies stage_dst(job, dst, ld, rows).  kKeep: cached stores, for an
+// output the next kernel reads straight back.
+template <class C, class Derived, bool kKeep = false>
 struct StagedCopyOut {
+  using Copy = StagedCopy<C, kKeep>;
   static constexpr bool kStaged = true;
-  using Drain = typename StagedCopy<C>::State;
-  static constexpr int kDrainCalls = StagedCopy<C>::kCalls;
+  using Drain = typename Copy::State;
+  static constexpr int kDrainCalls = Copy::kCalls;
   __device__ __forceinline__ void drain_setup(const Job<C>& j, Drain& d) const {
     bf16_t* dst[C::NB];
     int64_t ld;
     int rows;
     static_cast<const Derived*>(this)->stage_dst(j, dst, ld, rows);
-    StagedCopy<C>::setup(d, dst, ld, rows);
+    Copy::setup(d, dst, ld, rows);
   }
-  __device__ __forceinline__ void drain(Drain& d, const char* stg, int p) const { StagedCopy<C>::call(d, stg, p); }
-  __device__ __forceinline__ void drain_reset(Drain& d) const { StagedCopy<C>::reset(d); }
+  __device__ __forceinline__ void drain(Drain& d, const char* stg, int p) const { Copy::call(d, stg, p); }
+  __device__ __forceinline__ void drain_reset(Drain& d) const { Copy::reset(d); }
 };
 
 
