@@ -27,11 +27,21 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
 // Slot counts are a compile-time bound KT >= k (a power of two), so every
 // lane issues the loads of all of its token's rows before it needs them.
 
+// Chunks per lane per pass: a pass covers kPassCols columns of each row, as
+// kU 16-byte chunks per lane 512 columns apart, so a wave asks for up to
+// 4 KB of every row at once; at most 32 row chunks stay in registers.
+#ifndef MOE_COMBINE_U
+#define MOE_COMBINE_U 4
+#endif
+template <int KT>
+constexpr int kChunks = KT * MOE_COMBINE_U <= 32 ? MOE_COMBINE_U : (32 / KT > 0 ? 32 / KT : 1);
+
 // y[t] = sum_j g[t,j] o[row_of[t,j]]  (0 when the token has no rows).
 template <int KT>
 __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, const float* __restrict__ gates,
                                                  const int32_t* __restrict__ row_of, int T, int H, int k,
                                                  bf16_t* __restrict__ y) {
+  constexpr int kU = row_chunks<KT, 32>();
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -42,21 +52,29 @@ __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, c
     rows[j] = j < k ? row_of[static_cast<int64_t>(t) * k + j] : -1;
     g[j] = j < k ? gates[static_cast<int64_t>(t) * k + j] : 0.0f;
   }
-  for (int c = lane * 8; c < H; c += kWave * 8) {
-    uint4 v[KT];
+  for (int c0 = lane * 8; c0 < H; c0 += kWave * 8 * kU) {
+    uint4 v[KT][kU];
 #pragma unroll
     for (int j = 0; j < KT; ++j)
-      v[j] = rows[j] >= 0 ? *reinterpret_cast<const uint4*>(o + static_cast<int64_t>(rows[j]) * H + c)
-                          : make_uint4(0, 0, 0, 0);
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      float f[8];
-      unpack8(v[j], f);
+      for (int u = 0; u < kU; ++u) {
+        const int c = c0 + u * kWave * 8;
+        v[j][u] = (rows[j] >= 0 && c < H) ? *reinterpret_cast<const uint4*>(o + static_cast<int64_t>(rows[j]) * H + c)
+                                          : make_uint4(0, 0, 0, 0);
+      }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] += g[j] * f[i];
+    for (int u = 0; u < kU; ++u) {
+      const int c = c0 + u * kWave * 8;
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < KT; ++j) {
+        float f[8];
+        unpack8(v[j][u], f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += g[j] * f[i];
+      }
+      if (c < H) *reinterpret_cast<uint4*>(y + static_cast<int64_t>(t) * H + c) = pack8(acc);
     }
-    *reinterpret_cast<uint4*>(y + static_cast<int64_t>(t) * H + c) = pack8(acc);
   }
 }
 
@@ -65,6 +83,7 @@ template <int KT>
 __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ dy, const float* __restrict__ gates,
                                                      const int32_t* __restrict__ row_of, int T, int H, int k,
                                                      bf16_t* __restrict__ d_o) {
+  constexpr int kU = row_chunks<KT, 32>();
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -77,16 +96,24 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ 
   }
   if (rows[0] < 0) return;  // a masked token has no rows
   const bf16_t* dyr = dy + static_cast<int64_t>(t) * H;
-  for (int c = lane * 8; c < H; c += kWave * 8) {
-    float fy[8];
-    unpack8(*reinterpret_cast<const uint4*>(dyr + c), fy);
+  for (int c0 = lane * 8; c0 < H; c0 += kWave * 8 * kU) {
+    float fy[kU][8];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int c = c0 + u * kWave * 8;
+      unpack8(c < H ? *reinterpret_cast<const uint4*>(dyr + c) : make_uint4(0, 0, 0, 0), fy[u]);
+    }
 #pragma unroll
     for (int j = 0; j < KT; ++j) {
       if (rows[j] < 0) continue;
-      float out[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) out[i] = g[j] * fy[i];
-      *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(rows[j]) * H + c) = pack8(out);
+      for (int u = 0; u < kU; ++u) {
+        const int c = c0 + u * kWave * 8;
+        float out[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) out[i] = g[j] * fy[u][i];
+        if (c < H) *reinterpret_cast<uint4*>(d_o + static_cast<int64_t>(rows[j]) * H + c) = pack8(out);
+      }
     }
   }
 }

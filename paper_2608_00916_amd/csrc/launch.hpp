@@ -9,6 +9,15 @@
 
 namespace moe {
 
+// Row passes of the one-wave-per-token kernels (combine, its backward, the
+// router dX): a pass covers up to 4 KB of each of the token's KT rows, as
+// 16-byte chunks per lane 512 columns apart, with at most kBudget row chunks
+// held in registers per lane.
+template <int KT, int kBudget>
+constexpr int row_chunks() {
+  return 4 * KT <= kBudget ? 4 : (kBudget / KT > 0 ? kBudget / KT : 1);
+}
+
 // Rank-r adapters on every expert's gate/up and down projections (rank 0:
 // none): a1 [E,H,r], b1_gate / b1_up [E,r,F], a2 [E,F,r], b2 [E,r,H], and the
 // scale-multiplied rank-r intermediates P1 = scale Xp a1, P2 = scale A a2

@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void k_transpose_wr(const bf16_t* __restrict__
 // the k selected experts only, so the router term is k scaled rows of W_r^T
 // (L2-resident).  With kDense the router term is instead a precomputed row of
 // dz W_r^T (fp32 [T][H]; dz dense over E when the router losses are on).  One
-// wave per token, 8 columns per lane per pass.
+// wave per token; a pass takes row_chunks 16-byte chunks per lane of every row.
 template <int KT, bool kDense>
 __global__ __launch_bounds__(256) void k_router_dx(const float* __restrict__ dz_slot,
                                                    const int32_t* __restrict__ topk_idx,
@@ -99,42 +99,55 @@ __global__ __launch_bounds__(256) void k_router_dx(const float* __restrict__ dz_
     ex[j] = j < k ? topk_idx[p] : -1;
     dzs[j] = j < k ? dz_slot[p] : 0.0f;
   }
-  for (int c = lane * 8; c < H; c += kWave * 8) {
-    uint4 v[KT], w[KT];
+  // dXp and W_r^T rows both in registers: at k = 8 one chunk per row ran
+  // fastest (two took 186 registers and halved the waves per SIMD)
+  constexpr int kU = row_chunks<KT, 8>();
+  for (int c0 = lane * 8; c0 < H; c0 += kWave * 8 * kU) {
+    uint4 v[KT][kU], w[KT][kU];
 #pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      const bool on = rows[j] >= 0;
-      v[j] = on ? *reinterpret_cast<const uint4*>(dxp + static_cast<int64_t>(rows[j]) * H + c) : make_uint4(0, 0, 0, 0);
-      if constexpr (!kDense)
-        w[j] = on ? *reinterpret_cast<const uint4*>(w_rt + static_cast<int64_t>(ex[j]) * H + c) : make_uint4(0, 0, 0, 0);
-    }
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if constexpr (kDense) {
-      if (rows[0] >= 0) {  // a routed token: its dense router term
-        const float4 a = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c);
-        const float4 b = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c + 4);
-        acc[0] = a.x, acc[1] = a.y, acc[2] = a.z, acc[3] = a.w;
-        acc[4] = b.x, acc[5] = b.y, acc[6] = b.z, acc[7] = b.w;
+    for (int j = 0; j < KT; ++j)
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int c = c0 + u * kWave * 8;
+        const bool on = rows[j] >= 0 && c < H;
+        v[j][u] = on ? *reinterpret_cast<const uint4*>(dxp + static_cast<int64_t>(rows[j]) * H + c)
+                     : make_uint4(0, 0, 0, 0);
+        if constexpr (!kDense)
+          w[j][u] = on ? *reinterpret_cast<const uint4*>(w_rt + static_cast<int64_t>(ex[j]) * H + c)
+                       : make_uint4(0, 0, 0, 0);
       }
-    }
 #pragma unroll
-    for (int j = 0; j < KT; ++j) {
-      const uint32_t* pv = reinterpret_cast<const uint32_t*>(&v[j]);
-      const uint32_t* pw = reinterpret_cast<const uint32_t*>(&w[j]);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if constexpr (kDense) {
-          acc[2 * q] += lo_bf(pv[q]);
-          acc[2 * q + 1] += hi_bf(pv[q]);
-        } else {
-          acc[2 * q] += lo_bf(pv[q]) + dzs[j] * lo_bf(pw[q]);
-          acc[2 * q + 1] += hi_bf(pv[q]) + dzs[j] * hi_bf(pw[q]);
+    for (int u = 0; u < kU; ++u) {
+      const int c = c0 + u * kWave * 8;
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if constexpr (kDense) {
+        if (rows[0] >= 0 && c < H) {  // a routed token: its dense router term
+          const float4 a = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c);
+          const float4 b = *reinterpret_cast<const float4*>(dense + static_cast<int64_t>(t) * H + c + 4);
+          acc[0] = a.x, acc[1] = a.y, acc[2] = a.z, acc[3] = a.w;
+          acc[4] = b.x, acc[5] = b.y, acc[6] = b.z, acc[7] = b.w;
         }
       }
+#pragma unroll
+      for (int j = 0; j < KT; ++j) {
+        const uint32_t* pv = reinterpret_cast<const uint32_t*>(&v[j][u]);
+        const uint32_t* pw = reinterpret_cast<const uint32_t*>(&w[j][u]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if constexpr (kDense) {
+            acc[2 * q] += lo_bf(pv[q]);
+            acc[2 * q + 1] += hi_bf(pv[q]);
+          } else {
+            acc[2 * q] += lo_bf(pv[q]) + dzs[j] * lo_bf(pw[q]);
+            acc[2 * q + 1] += hi_bf(pv[q]) + dzs[j] * hi_bf(pw[q]);
+          }
+        }
+      }
+      if (c < H)
+        *reinterpret_cast<uint4*>(dx + static_cast<int64_t>(t) * H + c) =
+            make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                       pack_bf16x2(acc[6], acc[7]));
     }
-    *reinterpret_cast<uint4*>(dx + static_cast<int64_t>(t) * H + c) =
-        make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
-                   pack_bf16x2(acc[6], acc[7]));
   }
 }
 
