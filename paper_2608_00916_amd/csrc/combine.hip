@@ -142,13 +142,41 @@ struct RouterLossGrad {
 
 constexpr int kMaxPerLane = MOE_MAX_EXPERTS / kWave;
 
+// W_r^T for the router dX, built by extra workgroups of the gate backward
+// (independent work; a launch of its own cost more than the copy): tile b
+// of (H/32) x (E/32) 32 x 32 tiles, through LDS, w_rt[e][h] = w_r[h][e].
+struct WrTranspose {
+  const bf16_t* w_r = nullptr;
+  bf16_t* w_rt = nullptr;
+  int H = 0;
+};
+
+__device__ __forceinline__ void transpose_wr_tile(const WrTranspose& tr, int E, int b) {
+  __shared__ bf16_t tile[32][33];
+  const int th = cdiv(tr.H, 32);
+  const int h0 = (b % th) * 32, e0 = (b / th) * 32;
+  const int a = threadIdx.x >> 5, c = threadIdx.x & 31;
+#pragma unroll
+  for (int i = 0; i < 32; i += 8)
+    if (h0 + a + i < tr.H && e0 + c < E) tile[a + i][c] = tr.w_r[static_cast<int64_t>(h0 + a + i) * E + e0 + c];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 32; i += 8)
+    if (e0 + a + i < E && h0 + c < tr.H) tr.w_rt[static_cast<int64_t>(e0 + a + i) * tr.H + h0 + c] = tile[c][a + i];
+}
+
 template <int KT, bool kAux>
 __global__ __launch_bounds__(256) void k_gate_bwd(const float* __restrict__ part, int nparts,
                                                   const float* __restrict__ gates,
                                                   const int32_t* __restrict__ topk_idx,
                                                   const int32_t* __restrict__ row_of, int T, int E, int k,
                                                   float* __restrict__ dg_out, float* __restrict__ dz_slot,
-                                                  bf16_t* __restrict__ dz, RouterLossGrad rl) {
+                                                  bf16_t* __restrict__ dz, RouterLossGrad rl, WrTranspose tr) {
+  const int gate_blocks = cdiv(T, 4);
+  if (static_cast<int>(blockIdx.x) >= gate_blocks) {  // a W_r^T tile (whole workgroup)
+    transpose_wr_tile(tr, E, static_cast<int>(blockIdx.x) - gate_blocks);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
@@ -268,7 +296,16 @@ hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_
 hipError_t launch_gate_bwd(const float* part, int nparts, const float* gates, const int32_t* topk_idx,
                            const int32_t* row_of, int T, int E, int k, float* dg, float* dz_slot, bf16_t* dz,
                            const float* logits, const int32_t* counts, const int32_t* offsets, float aux_coef,
-                           float z_coef, hipStream_t s) {
+                           float z_coef, const bf16_t* w_r, int H, bf16_t* w_rt, hipStream_t s) {
+  WrTranspose tr;
+  int tr_blocks = 0;
+  if (w_r != nullptr) {
+    tr.w_r = w_r;
+    tr.w_rt = w_rt;
+    tr.H = H;
+    tr_blocks = cdiv(H, 32) * cdiv(E, 32);
+  }
+  const dim3 grid(cdiv(T, 4) + tr_blocks);
   RouterLossGrad rl;
   const bool aux = aux_coef != 0.0f || z_coef != 0.0f;
   if (aux) {
@@ -281,11 +318,11 @@ hipError_t launch_gate_bwd(const float* part, int nparts, const float* gates, co
   {
     TraceScope trace_scope(K_GATE_BWD, s);
     if (aux)
-      MOE_SLOT_DISPATCH2(k_gate_bwd, true, k, dim3(cdiv(T, 4)), s, part, nparts, gates, topk_idx, row_of, T, E, k, dg,
-                         dz_slot, dz, rl);
+      MOE_SLOT_DISPATCH2(k_gate_bwd, true, k, grid, s, part, nparts, gates, topk_idx, row_of, T, E, k, dg, dz_slot, dz,
+                         rl, tr);
     else
-      MOE_SLOT_DISPATCH2(k_gate_bwd, false, k, dim3(cdiv(T, 4)), s, part, nparts, gates, topk_idx, row_of, T, E, k,
-                         dg, dz_slot, dz, rl);
+      MOE_SLOT_DISPATCH2(k_gate_bwd, false, k, grid, s, part, nparts, gates, topk_idx, row_of, T, E, k, dg, dz_slot,
+                         dz, rl, tr);
   }
   return hipGetLastError();
 }

@@ -138,22 +138,24 @@ hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_
 // dz per slot (fp32 [T,k]) and dense over E (bf16 [T,E]).  With a non-zero
 // router-loss coefficient the dense dz also takes the router losses' gradient
 // (from the fp32 logits, the counts and offsets); dz per slot stays the gates'
-// part.
+// part.  With w_r non-null the same launch also writes w_rt = W_r^T ([E,H],
+// from W_r [H,E]) for the router dX, in workgroups of its own.
 hipError_t launch_gate_bwd(const float* part, int nparts, const float* gates, const int32_t* topk_idx,
                            const int32_t* row_of, int T, int E, int k, float* dg, float* dz_slot, bf16_t* dz,
                            const float* logits, const int32_t* counts, const int32_t* offsets, float aux_coef,
-                           float z_coef, hipStream_t s);
+                           float z_coef, const bf16_t* w_r, int H, bf16_t* w_rt, hipStream_t s);
 
 // ---- router backward (router_bwd.hip)
 int dwr_splits(int T);
 // dW_r = x^T dz via `dwr_splits(T)` fp32 partials in ws_f32 ([splits][H][E]).
 hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, float* ws_f32,
                       void* dw_r, bool f32_out, hipStream_t s);
-// dX[t] = sum_j (dXp[row_of[t,j]] + dz_j W_r[:, idx_j]); w_rt is [E,H] scratch.
-// With dz_dense (bf16 [T,E]) the router term is dz_dense W_r^T instead, formed
-// in `dense` (fp32 [T,H] scratch) by an MFMA product.
+// dX[t] = sum_j (dXp[row_of[t,j]] + dz_j W_r[:, idx_j]), with W_r^T in w_rt
+// ([E,H], written by launch_gate_bwd).  With dz_dense (bf16 [T,E]) the router
+// term is dz_dense W_r^T instead, formed in `dense` (fp32 [T,H] scratch) by an
+// MFMA product from w_r, and w_rt is not read.
 hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
                             const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
-                            bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s);
+                            const bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s);
 
 }  // namespace moe

@@ -462,7 +462,8 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   if (e != hipSuccess) return hip_status(e, "experts bwd");
   // gate gradients and dz from the down dgrad's <dA, A> sums
   e = launch_gate_bwd(w.dgate_part, dgate_parts(F), sv.gates, sv.topk_idx, sv.row_of, T, E, k, w.dgate, w.dz_slot,
-                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef,
+                      w.dense == nullptr ? static_cast<const bf16_t*>(w_r) : nullptr, H, w.w_rt, s);
   if (e != hipSuccess) return hip_status(e, "gate bwd");
   // dX right after dXp, while much of dXp is still in the last-level cache.
   e = launch_router_dx(w.dz_slot, sv.topk_idx, static_cast<const bf16_t*>(w_r), w.d_o, sv.row_of, T, H, E, k,
@@ -520,7 +521,8 @@ int moe_lora_bwd(const moe_dims* d, const void* x, const void* w_r, const void* 
   e = launch_down_dgrad(a, w.d_o, w.dg, w.du, lw.q2, s);
   if (e != hipSuccess) return hip_status(e, "down dgrad");
   e = launch_gate_bwd(w.dgate_part, dgate_parts(F), sv.gates, sv.topk_idx, sv.row_of, T, E, k, w.dgate, w.dz_slot,
-                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef, s);
+                      w.dz, sv.logits, sv.counts, sv.offsets, d->aux_loss_coef, d->z_loss_coef,
+                      w.dense == nullptr ? static_cast<const bf16_t*>(w_r) : nullptr, H, w.w_rt, s);
   if (e != hipSuccess) return hip_status(e, "gate bwd");
   // d a2 = A^T Q2 ([E][F][r]); d b2 = P2^T dO, formed as (dO^T P2)^T ([E][r][H])
   e = launch_lora_wgrad(a, sv.a, F, F, lw.q2, false, da2, f32, s);

@@ -44,34 +44,37 @@ __global__ __launch_bounds__(RTile::kThreads) void k_dwr_partial(const bf16_t* _
   }
 }
 
-// dW_r = sum over splits in order.
+// dW_r = sum over splits in order.  Four elements per thread (n % 4 == 0,
+// as H E is); each group of kGroup splits has its loads issued before its
+// adds, which still run in split order.
 template <bool F32>
 __global__ __launch_bounds__(256) void k_dwr_reduce(const float* __restrict__ partial, int splits,
                                                     int64_t n, void* __restrict__ dw_r) {
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+  constexpr int kGroup = 8;
+  const int64_t n4 = n / 4;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n4;
        i += static_cast<int64_t>(gridDim.x) * 256) {
-    float v = 0.0f;
-    for (int s = 0; s < splits; ++s) v += partial[static_cast<int64_t>(s) * n + i];
-    if constexpr (F32)
-      static_cast<float*>(dw_r)[i] = v;
-    else
-      static_cast<bf16_t*>(dw_r)[i] = f2bf(v);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < splits; s0 += kGroup) {
+      float4 p[kGroup];
+#pragma unroll
+      for (int g = 0; g < kGroup; ++g)
+        p[g] = s0 + g < splits ? reinterpret_cast<const float4*>(partial + static_cast<int64_t>(s0 + g) * n)[i]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int g = 0; g < kGroup; ++g) {
+        v.x += p[g].x;
+        v.y += p[g].y;
+        v.z += p[g].z;
+        v.w += p[g].w;
+      }
+    }
+    if constexpr (F32) {
+      reinterpret_cast<float4*>(dw_r)[i] = v;
+    } else {
+      reinterpret_cast<uint2*>(dw_r)[i] = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+    }
   }
-}
-
-// W_rT[E][H] = W_r[H][E] through 32 x 32 LDS tiles (grid H/32 x E/32).
-__global__ __launch_bounds__(256) void k_transpose_wr(const bf16_t* __restrict__ w_r, int H, int E,
-                                                      bf16_t* __restrict__ w_rt) {
-  __shared__ bf16_t tile[32][33];
-  const int h0 = blockIdx.x * 32, e0 = blockIdx.y * 32;
-  const int a = threadIdx.x >> 5, b = threadIdx.x & 31;
-#pragma unroll
-  for (int i = 0; i < 32; i += 8)
-    if (h0 + a + i < H && e0 + b < E) tile[a + i][b] = w_r[static_cast<int64_t>(h0 + a + i) * E + e0 + b];
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 32; i += 8)
-    if (e0 + a + i < E && h0 + b < H) w_rt[static_cast<int64_t>(e0 + a + i) * H + h0 + b] = tile[b][a + i];
 }
 
 // dX[t] = sum_j ( dXp[row_of[t,j]] + dz_j W_r[:, idx_j] ): dz is non-zero on
@@ -190,8 +193,8 @@ hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, fl
     hipLaunchKernelGGL(k_dwr_partial, dim3(splits, H / RTile::BM, cdiv(E, RTile::BN)), dim3(RTile::kThreads), 0, s, x, dz, T, H,
                        E, ws_f32);
   }
-  const int64_t n = static_cast<int64_t>(H) * E;
-  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(n, 256), 2048));
+  const int64_t n = static_cast<int64_t>(H) * E;  // a multiple of 4: E % 8 == 0
+  const int grid = static_cast<int>(std::min<int64_t>(cdiv64(n / 4, 256), 2048));
   if (f32_out) {
     TraceScope trace_scope(K_DWR_REDUCE, s);
     hipLaunchKernelGGL(k_dwr_reduce<true>, dim3(grid), dim3(256), 0, s, ws_f32, splits, n, dw_r);
@@ -204,15 +207,12 @@ hipError_t launch_dwr(const bf16_t* x, const bf16_t* dz, int T, int H, int E, fl
 
 hipError_t launch_router_dx(const float* dz_slot, const int32_t* topk_idx, const bf16_t* w_r,
                             const bf16_t* dxp, const int32_t* row_of, int T, int H, int E, int k,
-                            bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s) {
+                            const bf16_t* w_rt, bf16_t* dx, const bf16_t* dz_dense, float* dense, hipStream_t s) {
   const bool use_dense = dz_dense != nullptr;
   if (use_dense) {
     TraceScope trace_scope(K_ROUTER_DX_DENSE, s);
     hipLaunchKernelGGL(k_router_dx_dense, dim3(cdiv(T, RTile::BM), H / RTile::BN), dim3(RTile::kThreads), 0, s,
                        dz_dense, w_r, T, H, E, dense);
-  } else {
-    TraceScope trace_scope(K_TRANSPOSE_WR, s);
-    hipLaunchKernelGGL(k_transpose_wr, dim3(cdiv(H, 32), cdiv(E, 32)), dim3(256), 0, s, w_r, H, E, w_rt);
   }
   {
     TraceScope trace_scope(K_ROUTER_DX, s);

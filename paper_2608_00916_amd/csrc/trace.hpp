@@ -26,7 +26,6 @@ enum KernelId {
   K_DWR_REDUCE,
   K_ROUTER_DX,
   K_OFFSETS,
-  K_TRANSPOSE_WR,
   K_GATEUP_RECOMPUTE,
   K_ROUTER_LOSS,
   K_ROUTER_DX_DENSE,
