@@ -116,6 +116,9 @@ EDGE = {
     "top1": dict(T=200, H=128, E=8, k=1, F=128, seed=24),
     "k_equals_E": dict(T=130, H=128, E=8, k=8, F=256, seed=25),
     "max_E_max_k": dict(T=100, H=128, E=256, k=32, F=128, seed=26),
+    # 16-slot kernels with k < 16, and H = 640: a row pass of 1024 columns
+    # whose second chunk is masked past H
+    "k12_H640": dict(T=150, H=640, E=32, k=12, F=128, seed=28),
     # biased router: several experts receive no rows
     "empty_experts": dict(T=257, H=256, E=32, k=3, F=128, seed=27, zipf_s=1.2, n_cold=6),
 }

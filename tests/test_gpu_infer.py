@@ -17,6 +17,7 @@ CASES = {
     "ragged_multi_tile": dict(T=1000, H=512, E=8, k=2, F=384, seed=21),
     "single_token": dict(T=1, H=128, E=8, k=2, F=128, seed=23),
     "max_E_max_k": dict(T=100, H=128, E=256, k=32, F=128, seed=26),
+    "k12_H640": dict(T=150, H=640, E=32, k=12, F=128, seed=28),
     "empty_experts": dict(T=257, H=256, E=32, k=3, F=128, seed=27, zipf_s=1.2, n_cold=6),
     "masked": dict(T=333, H=256, E=16, k=2, F=128, seed=31),
 }
