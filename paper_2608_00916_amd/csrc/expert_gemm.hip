@@ -12,6 +12,7 @@
 #include "gemm_core.hpp"
 
 #include <algorithm>
+#include <mutex>
 
 namespace moe {
 
@@ -695,17 +696,20 @@ __global__ __launch_bounds__(P::C::kThreads) void k_stream(P prov) {
 inline int grid8(int64_t n) { return static_cast<int>(cdiv64(n, 8) * 8); }
 
 // Persistent grid: as many workgroups as can be resident on the device at
-// once (queried per kernel and device, then cached), rounded down to a
-// multiple of 8, and no more than the worst-case tile count needs.
+// once (queried per kernel and device, then cached; the cache is shared by
+// every host thread, under a lock), rounded down to a multiple of 8, and no
+// more than the worst-case tile count needs.
 int resident_workgroups(const void* kernel, int threads) {
   struct Entry {
     const void* kernel;
     int dev, blocks;
   };
+  static std::mutex lock;
   static Entry cache[64];
   static int used = 0;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  std::lock_guard<std::mutex> guard(lock);
   for (int i = 0; i < used; ++i)
     if (cache[i].kernel == kernel && cache[i].dev == dev) return cache[i].blocks;
   int cus = 0, per_cu = 0;
