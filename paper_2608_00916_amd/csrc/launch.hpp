@@ -98,14 +98,21 @@ hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_
 hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate,
                                        void* dw_up, bool dw_f32, hipStream_t s);
 
+// Tokens per chunk of the permutation's counting sort.
+constexpr int kPermChunk = 256;
+
 // ---- routing (router.hip)
 // logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
 // `part` (router_part_floats(T, E) floats) holds the partial sums of the
 // K-split logits product.  With aux_ws (router_loss_ws_floats(T, E) floats)
-// also the per-workgroup partial sums of the router losses.
+// also the per-workgroup partial sums of the router losses.  For the
+// permutation it also writes chunk_counts[c][e] (permute_ws_ints(T, E)
+// ints: rows of expert e among the tokens of chunk c, kPermChunk tokens per
+// chunk; integer atomic adds, so exact in any order) and sets
+// row_token[0, T k) to -1.
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
                              int E, int k, float* logits, float* part, int32_t* topk_idx, float* gates,
-                             float* aux_ws, hipStream_t s);
+                             float* aux_ws, int32_t* chunk_counts, int32_t* row_token, hipStream_t s);
 int64_t router_part_floats(int T, int E);
 int64_t router_loss_ws_floats(int T, int E);
 // out[0..1] = {L_aux, L_z} from those partial sums and the routing counts.
@@ -115,9 +122,10 @@ hipError_t launch_router_loss(const float* aux_ws, int T, int E, int k, const in
 // ---- permutation (permute.hip)
 // Workspace ints the permutation needs for T tokens and E experts.
 int64_t permute_ws_ints(int T, int E);
-// counts, offsets, tile_start, row_token (-1 beyond R), row_of from topk_idx;
-// then xp[r] = x[row_token[r]], written token-major through row_of (skipped
-// when xp is null).
+// counts, offsets, tile_start, row_token (-1 beyond R), row_of from topk_idx
+// and the chunk counts in ws that launch_router_fwd left (with row_token
+// already -1); then xp[r] = x[row_token[r]], written token-major through
+// row_of (skipped when xp is null).
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
                           int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s);

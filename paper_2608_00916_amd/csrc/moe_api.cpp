@@ -357,7 +357,8 @@ int block_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, sv.logits, fw.router_part, sv.topk_idx, sv.gates, fw.loss, s);
+                                   E, k, sv.logits, fw.router_part, sv.topk_idx, sv.gates, fw.loss, fw.perm,
+                                   sv.row_token, s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(sv.topk_idx, xb, T, H, E, k, sv.counts, sv.offsets, sv.tile_start, sv.tile_desc, sv.row_token,
                      sv.row_of, sv.xp, fw.perm, s);
@@ -567,7 +568,8 @@ int moe_infer(const moe_dims* d, const void* x, const void* w_r, const void* w_g
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   hipError_t e = launch_router_fwd(xb, static_cast<const bf16_t*>(w_r), masked ? token_mask : nullptr, T, H,
-                                   E, k, w.logits, w.router_part, w.topk_idx, w.gates, nullptr, s);
+                                   E, k, w.logits, w.router_part, w.topk_idx, w.gates, nullptr, w.perm, w.row_token,
+                                   s);
   if (e != hipSuccess) return hip_status(e, "router");
   e = launch_permute(w.topk_idx, xb, T, H, E, k, w.counts, w.offsets, w.tile_start, w.tile_desc, w.row_token, w.row_of,
                      w.xp, w.perm, s);

@@ -13,7 +13,7 @@ namespace moe {
 
 namespace {
 
-constexpr int kChunk = 256;  // tokens per workgroup (4 waves x 64 lanes)
+constexpr int kChunk = kPermChunk;  // tokens per workgroup (4 waves x 64 lanes)
 constexpr int kWords = kChunk / 64;
 
 // bits[e][w] bit l  <=>  token chunk*256 + 64 w + l selected expert e.
@@ -30,24 +30,6 @@ __device__ __forceinline__ void build_bits(unsigned long long (*bits)[kWords], c
     }
   }
   __syncthreads();
-}
-
-// Per chunk: rows of each expert; also marks every row_token slot unused (-1).
-__global__ __launch_bounds__(kChunk) void k_perm_hist(const int32_t* __restrict__ topk_idx, int T, int E,
-                                                      int k, int32_t* __restrict__ chunk_counts,
-                                                      int32_t* __restrict__ row_token) {
-  __shared__ unsigned long long bits[MOE_MAX_EXPERTS][kWords];
-  const int chunk = blockIdx.x;
-  const int t = chunk * kChunk + threadIdx.x;
-  if (t < T)
-    for (int j = 0; j < k; ++j) row_token[static_cast<int64_t>(t) * k + j] = -1;
-  build_bits(bits, topk_idx, T, E, k, chunk);
-  for (int e = threadIdx.x; e < E; e += kChunk) {
-    int c = 0;
-#pragma unroll
-    for (int w = 0; w < kWords; ++w) c += __popcll(bits[e][w]);
-    chunk_counts[static_cast<int64_t>(chunk) * E + e] = c;
-  }
 }
 
 // Exclusive scan of n values held one per thread (n <= blockDim = 256).
@@ -214,12 +196,7 @@ hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
                           int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
   const int nchunks = cdiv(T, kChunk);
-  int32_t* chunk_counts = ws;
-  {
-    TraceScope trace_scope(K_PERM_HIST, s);
-    hipLaunchKernelGGL(k_perm_hist, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts,
-                       row_token);
-  }
+  const int32_t* chunk_counts = ws;  // written by the router's top-k
   {
     TraceScope trace_scope(K_PERM_SCATTER, s);
     hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts, nchunks,

@@ -30,9 +30,13 @@ constexpr int kRouterSplits = 4;
 __global__ __launch_bounds__(RouterTile::kThreads) void k_router_logits(const bf16_t* __restrict__ x,
                                                                         const bf16_t* __restrict__ w_r, int T,
                                                                         int H, int E, float* __restrict__ logits,
-                                                                        float* __restrict__ part) {
+                                                                        float* __restrict__ part,
+                                                                        int32_t* __restrict__ zero, int n_zero) {
   using C = RouterTile;
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
+  // the permutation's chunk counts start at zero for the top-k's atomic adds
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < n_zero; i += C::kThreads) zero[i] = 0;
   const int t0 = blockIdx.x * kRouterTokens;
   const int rows = min(kRouterTokens, T - t0);
   const int split = blockIdx.y;
@@ -86,7 +90,8 @@ __device__ __forceinline__ int ballot_count(bool p) { return __popcll(__ballot(p
 // 0, below every logit's key, so they never count.  Returns the largest logit.
 template <int PL>
 __device__ __forceinline__ float topk_select(const float (&val)[PL], const uint32_t (&key)[PL], int k, int lane,
-                                             int32_t* __restrict__ idx_row, float* __restrict__ g_row) {
+                                             int32_t* __restrict__ idx_row, float* __restrict__ g_row,
+                                             int32_t* __restrict__ cnt_row) {
   uint32_t kth = 0u;  // largest P with #{key >= P} >= k
   for (int b = 31; b >= 0; --b) {
     const uint32_t cand = kth | (1u << b);
@@ -145,6 +150,7 @@ __device__ __forceinline__ float topk_select(const float (&val)[PL], const uint3
     if (sel[m]) {
       idx_row[slot[m]] = lane + kWave * m;
       g_row[slot[m]] = wm[m] / sum;
+      atomicAdd(cnt_row + lane + kWave * m, 1);
     }
   return top;
 }
@@ -159,7 +165,8 @@ template <int PL, bool kAux>
 __global__ __launch_bounds__(256) void k_topk(float* __restrict__ logits, const float* __restrict__ part,
                                               const uint8_t* __restrict__ mask, int T, int E, int k,
                                               int32_t* __restrict__ topk_idx, float* __restrict__ gates,
-                                              float* __restrict__ aux_part) {
+                                              float* __restrict__ aux_part, int32_t* __restrict__ chunk_counts,
+                                              int32_t* __restrict__ row_token) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int t = blockIdx.x * 4 + wv;
   if (!kAux && t >= T) return;
@@ -181,11 +188,15 @@ __global__ __launch_bounds__(256) void k_topk(float* __restrict__ logits, const 
         z[e] = v;
       }
       val[m] = v;
-      key[m] = e < E ? order_key(v) : 0u;
+      // a present expert's key stays above the padding key 0 (only a NaN
+      // with every bit set maps to 0), so a padding lane is never selected
+      key[m] = e < E ? max(order_key(v), 1u) : 0u;
     }
   }
+  if (t < T && lane < k) row_token[static_cast<int64_t>(t) * k + lane] = -1;
   if (on) {
-    topk_select<PL>(val, key, k, lane, topk_idx + static_cast<int64_t>(t) * k, gates + static_cast<int64_t>(t) * k);
+    topk_select<PL>(val, key, k, lane, topk_idx + static_cast<int64_t>(t) * k, gates + static_cast<int64_t>(t) * k,
+                    chunk_counts + static_cast<int64_t>(t / kPermChunk) * E);
   } else if (t < T && lane < k) {
     topk_idx[static_cast<int64_t>(t) * k + lane] = -1;
     gates[static_cast<int64_t>(t) * k + lane] = 0.0f;
@@ -271,18 +282,19 @@ int64_t router_part_floats(int T, int E) { return static_cast<int64_t>(kRouterSp
 
 hipError_t launch_router_fwd(const bf16_t* x, const bf16_t* w_r, const uint8_t* mask, int T, int H,
                              int E, int k, float* logits, float* part, int32_t* topk_idx, float* gates,
-                             float* aux_ws, hipStream_t s) {
+                             float* aux_ws, int32_t* chunk_counts, int32_t* row_token, hipStream_t s) {
   {
     TraceScope trace_scope(K_ROUTER_LOGITS, s);
     hipLaunchKernelGGL(k_router_logits, dim3(cdiv(T, kRouterTokens), kRouterSplits), dim3(RouterTile::kThreads), 0,
-                       s, x, w_r, T, H, E, logits, part);
+                       s, x, w_r, T, H, E, logits, part, chunk_counts, static_cast<int>(permute_ws_ints(T, E)));
   }
   {
     TraceScope trace_scope(K_TOPK, s);
     const dim3 grid(cdiv(T, 4)), block(256);
     // experts per lane: 1, 2 or 4 (E <= 256)
 #define MOE_TOPK(PL, AUX) \
-  hipLaunchKernelGGL((k_topk<PL, AUX>), grid, block, 0, s, logits, part, mask, T, E, k, topk_idx, gates, aux_ws)
+  hipLaunchKernelGGL((k_topk<PL, AUX>), grid, block, 0, s, logits, part, mask, T, E, k, topk_idx, gates, aux_ws, \
+                     chunk_counts, row_token)
     const bool aux = aux_ws != nullptr;
     if (E <= kWave) {
       if (aux) MOE_TOPK(1, true); else MOE_TOPK(1, false);

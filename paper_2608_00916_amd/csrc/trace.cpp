@@ -32,7 +32,7 @@ hipEvent_t take_event() {
 }
 
 const char* const kNames[K_NUM_KERNELS] = {
-    "router_logits", "topk",         "perm_hist",     "perm_scatter", "permute_rows",
+    "router_logits", "topk",         "perm_scatter", "permute_rows",
     "gateup_fwd",    "down_fwd",     "combine",       "combine_bwd",  "down_dgrad_swiglu",
     "down_wgrad",    "gateup_dgrad", "gateup_wgrad",  "dwr_partial",  "dwr_reduce",   "router_dx",
     "offsets_from_counts", "gateup_recompute", "router_loss", "router_dx_dense", "lora_rows", "lora_wgrad",

@@ -11,7 +11,6 @@ namespace moe {
 enum KernelId {
   K_ROUTER_LOGITS,
   K_TOPK,
-  K_PERM_HIST,
   K_PERM_SCATTER,
   K_PERMUTE_ROWS,
   K_GATEUP_FWD,
