@@ -133,6 +133,32 @@ def test_edge_shapes(case):
     compare(inp, gpu_run(inp), f, b)
 
 
+def test_nan_token():
+    """One token's hidden row is NaN, so all its logits are NaN.  The top-k
+    works on integer order keys: the token still gets k distinct experts in
+    [0, E), and the permutation stays the valid stable one of that selection.
+    No other token changes: their routing and outputs match the oracle run
+    with that row zeroed (rows never mix in the forward)."""
+    inp = workloads.block_inputs(T=300, H=256, E=16, k=4, F=128, seed=61)
+    d = inp["dims"]
+    bad = 7
+    x = inp["x"].copy()
+    x[bad] = 0x7FC0  # bf16 quiet NaN
+    g = gpu_run(dict(inp, x=x))
+    idx = g["topk_idx"]
+    assert np.all((idx >= 0) & (idx < d["E"]))
+    assert len(set(idx[bad].tolist())) == d["k"]
+    check_permutation_valid(idx, g["counts"], g["offsets"], g["row_token"], g["row_of"], d["E"])
+    x0 = inp["x"].copy()
+    x0[bad] = 0
+    f, _ = oracle_run(dict(inp, x=x0))
+    o = np.arange(d["T"]) != bad
+    _, _, flipped = check_routing(f["z"][o], f["idx"][o], f["gates"][o], g["logits"][o], idx[o],
+                                  g["gates"][o], d["k"])
+    assert np.all(np.isfinite(g["y"][o]))
+    assert_close("y", g["y"][o][~flipped], f["Y"][o][~flipped])
+
+
 def test_underflowing_gates():
     """Router logits far apart (W_r scaled up 1000x): many second gates are
     exactly 0 in fp32.  The gate gradient then takes its g = 0 branch
