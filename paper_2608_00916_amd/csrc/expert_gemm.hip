@@ -69,38 +69,45 @@ struct LoraSeg {
 // with X_s K-contiguous ([rows][K], ld ldx) and W_s per expert (e * estride):
 // MN-contiguous [K][rank] (the a matrices) or, with B_KC, K-contiguous rows q
 // of length K ([rank][K], the b matrices).  NSEG = 2 sums two segments (dG with
-// b1_gate and dU with b1_up).  2 waves of 64 x 16.
-using LoraRows = Tile<128, 16, 1, 2, 1>;
+// b1_gate and dU with b1_up).  These stream whole activation matrices through
+// a rank-16 product, so they are bound by memory: one wave per 64-row half of
+// a 128-row tile (64 x 16), twice the workgroups of whole tiles, keeps twice
+// the rows in flight per CU.
+using LoraRows = Tile<64, 16, 1, 1, 1>;
 template <bool B_KC, int NSEG>
 __global__ __launch_bounds__(LoraRows::kThreads) void k_lora_rows(
     const bf16_t* __restrict__ x0, const bf16_t* __restrict__ x1, int64_t ldx, const bf16_t* __restrict__ w0,
     const bf16_t* __restrict__ w1, int64_t estride, int K, const int32_t* __restrict__ tile_start,
     const int2* __restrict__ tile_desc, int E, int rank, float scale, bf16_t* __restrict__ out) {
   using C = LoraRows;
-  static_assert(C::BM == kRowTile, "grouped products tile rows in units of kRowTile");
+  constexpr int kHalves = kRowTile / C::BM;
+  static_assert(kHalves * C::BM == kRowTile, "a row tile splits into whole halves");
   __shared__ __attribute__((aligned(16))) char smem[C::kLds];
-  for_each_grouped_tile(tile_start, tile_desc, E, rank / C::BN, [&](const MTile& t) {
+  for_each_grouped_tile(tile_start, tile_desc, E, rank / C::BN * kHalves, [&](const MTile& t) {
+    const int half = t.nt % kHalves;
+    const int m0 = t.m0 + half * C::BM;
+    const int m_lim = min(C::BM, t.m_lim - half * C::BM);
+    if (m_lim <= 0) return;  // the empty second half of a short tile (the whole wave)
     f32x4 acc[C::FM][C::FN];
     zero_acc<C>(acc);
-    const int q0 = t.nt * C::BN;
+    const int q0 = (t.nt / kHalves) * C::BN;
     const int64_t wofs = static_cast<int64_t>(t.e) * estride + (B_KC ? static_cast<int64_t>(q0) * K : q0);
     const int64_t ldw = B_KC ? K : rank;
     const bf16_t* b0[1] = {w0 + wofs};
-    gemm_mainloop<C, true, B_KC>(x0 + static_cast<int64_t>(t.m0) * ldx, ldx, t.m_lim, b0, ldw, C::BN, K, smem, acc);
+    gemm_mainloop<C, true, B_KC>(x0 + static_cast<int64_t>(m0) * ldx, ldx, m_lim, b0, ldw, C::BN, K, smem, acc);
     if constexpr (NSEG == 2) {
       const bf16_t* b1[1] = {w1 + wofs};
-      gemm_mainloop<C, true, B_KC>(x1 + static_cast<int64_t>(t.m0) * ldx, ldx, t.m_lim, b1, ldw, C::BN, K, smem,
-                                   acc);
+      gemm_mainloop<C, true, B_KC>(x1 + static_cast<int64_t>(m0) * ldx, ldx, m_lim, b1, ldw, C::BN, K, smem, acc);
     }
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int mi = 0; mi < C::FM; ++mi) {
       const int r = frag_row<C>(mi, lane);
-      if (r >= t.m_lim) continue;
+      if (r >= m_lim) continue;
       f32x4 v = acc[mi][0];
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] *= scale;
-      *reinterpret_cast<uint2*>(out + static_cast<int64_t>(t.m0 + r) * rank + q0 + frag_col<C>(0, lane)) =
+      *reinterpret_cast<uint2*>(out + static_cast<int64_t>(m0 + r) * rank + q0 + frag_col<C>(0, lane)) =
           pack4_bf16(v);
     }
   });
@@ -916,7 +923,8 @@ hipError_t launch_lora_rows(const ExpertArgs& a, const bf16_t* x0, const bf16_t*
                             const bf16_t* w0, const bf16_t* w1, int64_t estride, int K, bool b_kc, bf16_t* out,
                             hipStream_t s) {
   using C = LoraRows;
-  const int64_t tiles = static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.lora.rank / C::BN);
+  const int64_t tiles =
+      static_cast<int64_t>(max_row_tiles(a.rows_cap, a.E)) * (a.lora.rank / C::BN) * (kRowTile / C::BM);
   TraceScope trace_scope(K_LORA_ROWS, s);
 #define MOE_LORA_ROWS(KC, NS)                                                                                   \
   do {                                                                                                          \
