@@ -70,9 +70,8 @@ struct LoraSeg {
 // MN-contiguous [K][rank] (the a matrices) or, with B_KC, K-contiguous rows q
 // of length K ([rank][K], the b matrices).  NSEG = 2 sums two segments (dG with
 // b1_gate and dU with b1_up).  These stream whole activation matrices through
-// a rank-16 product, so they are bound by memory: one wave per 64-row half of
-// a 128-row tile (64 x 16), twice the workgroups of whole tiles, keeps twice
-// the rows in flight per CU.
+// a rank-16 product, so they are bound by memory; one wave takes one 64-row
+// half of a 128-row tile (64 x 16).
 using LoraRows = Tile<64, 16, 1, 1, 1>;
 template <bool B_KC, int NSEG>
 __global__ __launch_bounds__(LoraRows::kThreads) void k_lora_rows(
