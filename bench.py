@@ -10,8 +10,11 @@ resident in HBM before the timed region.  Prints one JSON line.
 The workload defaults to the Qwen3-30B-A3B-shaped layer on one GPU (T=8192
 tokens, H=2048, E=128 experts, top-8, F=768, bf16).  The dominant kernel's
 roofline comes from HIP events recorded around every library kernel launch
-over the timed region; the CPU baseline is the fp64 oracle on a bounded
-sample of the same workload, timed on this host's cores.
+over a second pass of the timed steps.  The Zipf-routed (T=32768) and the
+masked long-passage (T=65536) workloads are timed after it as extra lines.
+The CPU baseline is the oracle's fp32 instance on a bounded sample of the main
+workload, timed on this host's cores; the same sample through the fp64
+oracle gives the parity block (near ties, flips, per-tensor errors).
 """
 from __future__ import annotations
 
@@ -135,24 +138,91 @@ def stored_traffic(workload, kernel):
     return None if k is None else k["hbm_bytes"]
 
 
-def cpu_baseline(inp, k, tokens):
-    """The fp64 oracle, as it stands, on the first `tokens` tokens."""
+def host_cores():
+    """Cores this process may run on (its affinity mask), the host's share."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_baseline(inp, k, tokens, gpu=None):
+    """The CPU baseline leg: the oracle, as it stands, on the first `tokens`
+    tokens of the workload.
+
+    Timed: the oracle's fp32 instance (inputs widened to float32), one
+    fwd+bwd.  Then, with `gpu` (host copies of the GPU's routing, Y, dX and
+    gradients of the timed step), the same sample through the fp64 instance is
+    the reference of a parity block: near ties (set / order), tokens whose
+    expert set flipped, whether the routing tables are bit-exact, and the
+    per-tensor max-relative errors of Y and dX on the sample (forward and dX
+    are separable over tokens) and, when the sample is the whole batch, of
+    dW_r and every expert's weight gradients."""
     from threadpoolctl import threadpool_info
 
     from oracle import moe_oracle as O
-    w = {n: O.widen_bf16(inp[n]) for n in ("w_r", "w_gate", "w_up", "w_down")}
+    names = ("w_r", "w_gate", "w_up", "w_down")
+    mask = None if inp["mask"] is None else inp["mask"][:tokens].astype(bool)
+    w32 = {n: O.widen_bf16(inp[n], np.float32) for n in names}
+    x32 = O.widen_bf16(inp["x"][:tokens], np.float32)
+    dy32 = O.widen_bf16(inp["dy"][:tokens], np.float32)
+    t0 = time.perf_counter()
+    f = O.moe_forward(x32, w32["w_r"], w32["w_gate"], w32["w_up"], w32["w_down"], k, mask)
+    O.moe_backward(x32, w32["w_r"], w32["w_gate"], w32["w_up"], w32["w_down"], f, dy32)
+    dt = time.perf_counter() - t0
+    del w32, x32, dy32, f
+    blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    T = inp["dims"]["T"]
+    out = {"value": tokens / dt, "unit": "tokens/s", "cores": host_cores(), "blas_threads": int(blas),
+           "kind": "oracle",
+           "sample": f"first {tokens} of {T} tokens of the same workload (all {inp['dims']['E']} experts' "
+                     f"weights), one fwd+bwd, the oracle's fp32 instance, {dt:.1f} s"}
+    if gpu is None:
+        return out, None
+    w = {n: O.widen_bf16(inp[n]) for n in names}
     x = O.widen_bf16(inp["x"][:tokens])
     dy = O.widen_bf16(inp["dy"][:tokens])
-    mask = None if inp["mask"] is None else inp["mask"][:tokens].astype(bool)
-    t0 = time.perf_counter()
     f = O.moe_forward(x, w["w_r"], w["w_gate"], w["w_up"], w["w_down"], k, mask)
-    O.moe_backward(x, w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, dy)
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {tokens} of {inp['dims']['T']} tokens of the same workload "
-                      f"(all {inp['dims']['E']} experts' weights), one fwd+bwd, fp64, "
-                      f"{dt:.1f} s"}
+    b = O.moe_backward(x, w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, dy)
+    return out, parity_block(O, f, b, gpu, k, tokens, T, mask)
+
+
+def max_rel(got, ref):
+    scale = float(np.abs(ref).max())
+    d = float(np.abs(np.asarray(got, dtype=np.float64) - ref).max()) if ref.size else 0.0
+    return d / scale if scale > 0 else d
+
+
+def parity_block(O, f, b, gpu, k, tokens, T, mask):
+    """Agreement of the timed step's GPU outputs with the fp64 oracle on the
+    CPU-baseline sample (the first `tokens` tokens)."""
+    E = f["z"].shape[1]
+    st, ot = O.near_ties(f["z"], k, gap=1e-4, mask=mask)
+    gidx = gpu["topk_idx"][:tokens]
+    valid = np.ones(tokens, dtype=bool) if mask is None else mask
+    flipped = np.array([set(a) != set(c) for a, c in zip(gidx.tolist(), f["idx"].tolist())]) & valid
+    clean = valid & ~st & ~ot
+    res = {"reference": "oracle fp64", "tokens": tokens, "tie_gap": 1e-4,
+           "near_ties_set": int(st.sum()), "near_ties_order": int(ot.sum()), "flipped": int(flipped.sum()),
+           "experts_bit_exact_off_ties": bool(np.array_equal(gidx[clean], f["idx"][clean]))}
+    keep = ~flipped
+    res["y_max_rel"] = max_rel(gpu["y"][:tokens][keep], f["Y"][keep])
+    res["dx_max_rel"] = max_rel(gpu["dx"][:tokens][keep], b["dx"][keep])
+    if tokens == T:  # the whole batch: routing tables and weight gradients too
+        same = not flipped.any()
+        res["counts_offsets_bit_exact"] = bool(same and np.array_equal(gpu["counts"], f["counts"])
+                                               and np.array_equal(gpu["offsets"], f["offsets"]))
+        res["row_token_bit_exact"] = bool(same and np.array_equal(gpu["row_token"], f["row_token"]))
+        touched = np.zeros(E, dtype=bool)
+        for t in np.nonzero(flipped)[0]:
+            touched[[e for e in list(gidx[t]) + list(f["idx"][t]) if e >= 0]] = True
+        cols = ~touched
+        res["dw_r_max_rel"] = max_rel(gpu["dw_r"][:, cols], b["dw_r"][:, cols])
+        for n in ("dw_gate", "dw_up", "dw_down"):
+            res[n + "_max_rel"] = max(max_rel(gpu[n](e), b[n][e]) for e in np.nonzero(cols)[0])
+        res["experts_compared"] = int(cols.sum())
+    res["within_2e-2"] = all(v <= 2e-2 for n, v in res.items() if n.endswith("_max_rel"))
+    return res
 
 
 def serving_forward(moe, t, tm, T, H, E, F, k, Tv, steps, warmup):
@@ -250,6 +320,160 @@ def ep_share_step(moe, steps, warmup):
             "tflops": 18.0 * H * F * R / (ms * 1e-3) / 1e12}
 
 
+GEMM_NAMES = ("gateup_fwd", "down_fwd", "down_dgrad_swiglu", "down_wgrad", "gateup_dgrad", "gateup_wgrad")
+
+
+def kernel_table(kern, workload, T, Tv, H, E, F, k, R):
+    """Per-kernel average launch time and achieved rate, the grouped products'
+    fraction of the bf16 peak, and the dominant kernel's roofline."""
+    per = {}
+    for name, (tot, n) in kern.items():
+        avg_ms = tot / n
+        kind, amt = kernel_work(name, T, Tv, H, E, F, k, R)
+        row = {"avg_us": round(avg_ms * 1e3, 2), "launches": n}
+        if kind == "flop":
+            row["tflops"] = round(amt / (avg_ms * 1e-3) / 1e12, 1)
+        elif kind == "byte":
+            row["gbs"] = round(amt / (avg_ms * 1e-3) / 1e9, 1)
+        per[name] = row
+    out = {"kernels": per}
+    gemm_ms = sum(kern[n][0] / kern[n][1] for n in GEMM_NAMES if n in kern)
+    out["grouped_gemm_frac_bf16_peak"] = 18.0 * H * F * R / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+    dom = max(kern, key=lambda n: kern[n][0])
+    tot, n = kern[dom]
+    avg_s = tot / n * 1e-3
+    kind, amt = kernel_work(dom, T, Tv, H, E, F, k, R)
+    traffic = stored_traffic(workload, dom)
+    if kind == "flop":
+        ach = amt / avg_s / 1e12
+        out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic}
+    else:
+        ach = amt / avg_s / 1e9
+        out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+    return out
+
+
+def time_block(moe, name, steps, warmup, trace, copy_mib=0, keep=False):
+    """Times `steps` fwd+bwd steps of block workload `name` after `warmup`
+    untimed ones (inputs resident in HBM), then, with `trace`, the same steps
+    again with per-launch HIP events.  Returns (result dict, state), state
+    holding the inputs and the block when `keep`."""
+    import torch
+    cfg = workloads.CONFIGS[name]
+    inp = workloads.make(name)
+    d = inp["dims"]
+    T, H, E, F, k = d["T"], d["H"], d["E"], d["F"], d["k"]
+    mask_np = inp["mask"]
+    Tv = T if mask_np is None else int(mask_np.sum())
+    R = Tv * k
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+    t = {n: dev(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    tm = None if mask_np is None else torch.from_numpy(mask_np.astype(np.uint8)).cuda()
+    blk = moe.MoEBlock(T, H, E, F, k, mask=tm is not None)
+
+    if copy_mib:
+        n = copy_mib * 2 ** 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    def step(marks=None):
+        if marks:
+            marks[0].record()
+        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
+        if marks:
+            marks[1].record()
+        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
+        if marks:
+            marks[2].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {name}: warmup {warmup} done", file=sys.stderr, flush=True)
+
+    # Timed region: exactly `steps` steps, bracketed by synchronisations,
+    # without per-kernel events (three events per step give the fwd/bwd split).
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record()
+    for i in range(steps):
+        step(marks[i])
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = ev0.elapsed_time(ev1) / steps
+    print(f"[bench] {name}: timed {steps} steps: {ms:.3f} ms/step (wall {1e3 * wall / steps:.3f})",
+          file=sys.stderr, flush=True)
+
+    def pct(v):
+        q = np.percentile(np.asarray(v), [10, 50, 90])
+        return {"p10": round(float(q[0]), 4), "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4)}
+    res = {"ms_per_step": ms, "tokens_per_s": Tv / (ms * 1e-3),
+           "config": {"workload": f"{name} MoE block fwd+bwd", "T": T, "T_valid": Tv, "H": H, "E": E,
+                      "top_k": k, "F": F, "routed_rows": R, "seed": cfg["seed"]},
+           "block_tflops": (18.0 * H * F * R + 6.0 * H * E * Tv) / (ms * 1e-3) / 1e12,
+           "timing": {"fwd_ms": pct([m[0].elapsed_time(m[1]) for m in marks]),
+                      "bwd_ms": pct([m[1].elapsed_time(m[2]) for m in marks]),
+                      "step_ms": pct([m[0].elapsed_time(m[2]) for m in marks])}}
+    res["block_frac_bf16_peak"] = res["block_tflops"] / PEAK_BF16_TFLOPS
+    if mask_np is not None:
+        res["valid_fraction"] = Tv / T
+
+    # Kernel region: the same steps again with the library's per-launch HIP
+    # events (recorded on the launch stream around every kernel), for the
+    # per-kernel table and the roofline.  The events themselves lengthen a
+    # step by a few percent, which is why they stay out of the timed region.
+    if trace:
+        moe.moe_trace_read()  # drop anything recorded before
+        moe.moe_trace_enable(True)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        moe.moe_trace_enable(False)
+        kern = moe.moe_trace_read()
+        res["kernel_region_ms_per_step"] = e0.elapsed_time(e1) / steps
+        print(f"[bench] {name}: kernel region {res['kernel_region_ms_per_step']:.3f} ms/step with per-kernel "
+              f"events", file=sys.stderr, flush=True)
+        if kern:
+            res.update(kernel_table(kern, name, T, Tv, H, E, F, k, R))
+    state = dict(inp=inp, t=t, tm=tm, blk=blk, dims=(T, H, E, F, k, Tv)) if keep else None
+    if not keep:
+        del t, tm, blk
+        torch.cuda.empty_cache()
+    return res, state
+
+
+def gpu_outputs(blk):
+    """Host copies of the last step's routing, Y, dX and dW_r; the expert
+    weight gradients are copied one expert at a time on demand."""
+    def h(t):
+        if t.dtype in (__import__("torch").bfloat16, __import__("torch").float32):
+            return t.float().cpu().numpy().astype(np.float64)
+        return t.cpu().numpy().astype(np.int64)
+    v = blk.views
+    out = {n: h(v[n]) for n in ("topk_idx", "counts", "offsets", "row_token")}
+    out.update(y=h(blk.y), dx=h(blk.dx), dw_r=h(blk.dw_r))
+    for n in ("dw_gate", "dw_up", "dw_down"):
+        out[n] = (lambda g: (lambda e: h(g[e])))(getattr(blk, n))
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -267,6 +491,9 @@ def main():
     ap.add_argument("--no-ep-share", action="store_true",
                     help="skip the EP-share timing (its expert products have another shape, so a kernel "
                          "trace of the block leaves it out)")
+    ap.add_argument("--extra-workloads", default="zipf,long_passage",
+                    help="comma-separated block workloads timed after the main one ('' = none)")
+    ap.add_argument("--extra-steps", type=int, default=20, help="timed steps of each extra workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run one torch copy of MIB MiB before the steps (counter calibration)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -284,155 +511,53 @@ def main():
 
     import paper_2608_00916_amd as moe
 
-    cfg = workloads.CONFIGS[args.workload]
-    inp = workloads.make(args.workload)
-    d = inp["dims"]
-    T, H, E, F, k = d["T"], d["H"], d["E"], d["F"], d["k"]
-    mask_np = inp["mask"]
-    Tv = T if mask_np is None else int(mask_np.sum())
-    R = Tv * k
-
-    def dev(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
-
-    t = {n: dev(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
-    tm = None if mask_np is None else torch.from_numpy(mask_np.astype(np.uint8)).cuda()
-    blk = moe.MoEBlock(T, H, E, F, k, mask=tm is not None)
-
-    if args.copy_calibration:
-        n = args.copy_calibration * 2 ** 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    def step(marks=None):
-        if marks:
-            marks[0].record()
-        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
-        if marks:
-            marks[1].record()
-        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
-        if marks:
-            marks[2].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print(f"[bench] {args.workload}: warmup {args.warmup} done", file=sys.stderr, flush=True)
-
-    # Timed region: exactly K steps, bracketed by synchronisations, without
-    # per-kernel events (three events per step give the fwd/bwd split).
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    ev0.record()
-    for i in range(args.steps):
-        step(marks[i])
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step (wall {1e3 * wall / args.steps:.3f})",
-          file=sys.stderr, flush=True)
-
-    # Kernel region: the same K steps again with the library's per-launch HIP
-    # events (recorded on the launch stream around every kernel), for the
-    # per-kernel table and the roofline.  The events themselves lengthen a
-    # step by a few percent, which is why they stay out of the timed region.
-    kern = {}
-    traced_ms = None
-    if not args.no_trace:
-        moe.moe_trace_read()  # drop anything recorded before
-        moe.moe_trace_enable(True)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record()
-        for _ in range(args.steps):
-            step()
-        e1.record()
-        torch.cuda.synchronize()
-        moe.moe_trace_enable(False)
-        kern = moe.moe_trace_read()
-        traced_ms = e0.elapsed_time(e1) / args.steps
-        print(f"[bench] kernel region: {traced_ms:.3f} ms/step with per-kernel events", file=sys.stderr,
-              flush=True)
-
-    def pct(v):
-        q = np.percentile(np.asarray(v), [10, 50, 90])
-        return {"p10": round(float(q[0]), 4), "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4)}
-    timing = {"fwd_ms": pct([m[0].elapsed_time(m[1]) for m in marks]),
-              "bwd_ms": pct([m[1].elapsed_time(m[2]) for m in marks]),
-              "step_ms": pct([m[0].elapsed_time(m[2]) for m in marks])}
+    res, st = time_block(moe, args.workload, args.steps, args.warmup, not args.no_trace,
+                         copy_mib=args.copy_calibration, keep=True)
+    T, H, E, F, k, Tv = st["dims"]
+    t, tm = st["t"], st["tm"]
     forward_only = None if args.no_forward_only else serving_forward(moe, t, tm, T, H, E, F, k, Tv, args.steps,
                                                                      args.warmup)
     lora = None if args.no_forward_only else lora_step(moe, t, tm, T, H, E, F, k, Tv, args.lora_rank,
                                                        args.steps, args.warmup)
-    ep = None if (args.no_forward_only or args.no_ep_share) else ep_share_step(moe, args.steps, args.warmup)
-
-    gemm_flop = 18.0 * H * F * R
-    router_flop = 6.0 * H * E * Tv
-    tflops = (gemm_flop + router_flop) / (ms * 1e-3) / 1e12
     out = {
         "metric": METRIC,
-        "value": Tv / (ms * 1e-3),
+        "value": res["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload} MoE block fwd+bwd", "T": T, "T_valid": Tv, "H": H,
-                   "E": E, "top_k": k, "F": F, "routed_rows": R, "seed": cfg["seed"]},
-        "block_tflops": tflops,
-        "block_frac_bf16_peak": tflops / PEAK_BF16_TFLOPS,
-        "timing": timing,
-        "forward_only": forward_only,
-        "expert_lora": lora,
-        "ep_share": ep,
+        "config": res["config"],
     }
-    if traced_ms is not None:
-        out["kernel_region_ms_per_step"] = traced_ms
-    if kern:
-        per = {}
-        for name, (tot, n) in kern.items():
-            avg_ms = tot / n
-            kind, amt = kernel_work(name, T, Tv, H, E, F, k, R)
-            row = {"avg_us": round(avg_ms * 1e3, 2), "launches": n}
-            if kind == "flop":
-                row["tflops"] = round(amt / (avg_ms * 1e-3) / 1e12, 1)
-            elif kind == "byte":
-                row["gbs"] = round(amt / (avg_ms * 1e-3) / 1e9, 1)
-            per[name] = row
-        out["kernels"] = per
-        gemm_names = ("gateup_fwd", "down_fwd", "down_dgrad_swiglu", "down_wgrad", "gateup_dgrad",
-                      "gateup_wgrad")
-        gemm_ms = sum(kern[n][0] / kern[n][1] for n in gemm_names if n in kern)
-        out["grouped_gemm_frac_bf16_peak"] = gemm_flop / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
-        dom = max(kern, key=lambda n: kern[n][0])
-        tot, n = kern[dom]
-        avg_s = tot / n * 1e-3
-        kind, amt = kernel_work(dom, T, Tv, H, E, F, k, R)
-        traffic = stored_traffic(args.workload, dom)
-        if kind == "flop":
-            ach = amt / avg_s / 1e12
-            out["roofline"] = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
-                               "unit": "TFLOP/s", "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic}
-        else:
-            ach = amt / avg_s / 1e9
-            out["roofline"] = {"kernel": dom, "bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS,
-                               "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+    for n in ("block_tflops", "block_frac_bf16_peak", "valid_fraction", "timing", "kernel_region_ms_per_step",
+              "kernels", "grouped_gemm_frac_bf16_peak", "roofline"):
+        if n in res:
+            out[n] = res[n]
+    out["forward_only"] = forward_only
+    out["expert_lora"] = lora
+    gpu = gpu_outputs(st["blk"]) if args.cpu_tokens > 0 else None
+    inp = st["inp"]
+    del st, t, tm
+    torch.cuda.empty_cache()
+    out["ep_share"] = None if (args.no_forward_only or args.no_ep_share) else ep_share_step(moe, args.steps,
+                                                                                             args.warmup)
+    extra = {}
+    for name in [n for n in args.extra_workloads.split(",") if n and n != args.workload]:
+        r, _ = time_block(moe, name, args.extra_steps, min(args.warmup, 5), not args.no_trace)
+        extra[name] = {n: r[n] for n in ("ms_per_step", "tokens_per_s", "config", "block_tflops",
+                                         "block_frac_bf16_peak", "valid_fraction", "grouped_gemm_frac_bf16_peak",
+                                         "roofline", "kernels") if n in r}
+        extra[name]["steps"] = args.extra_steps
+    if extra:
+        out["extra_workloads"] = extra
     if args.cpu_tokens > 0:
         print(f"[bench] CPU baseline: oracle on {args.cpu_tokens} tokens", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(inp, k, min(args.cpu_tokens, T))
+        out["cpu_baseline"], out["parity"] = cpu_baseline(inp, k, min(args.cpu_tokens, T), gpu)
     print(json.dumps(out), flush=True)
 
 

@@ -24,8 +24,11 @@ dropless top-k MoE with SwiGLU experts, under these readings:
 * the router gradient flows through the gates only (the selection is
   piecewise constant).
 
-Everything is float64.  bf16 inputs arrive as uint16 bit patterns and are
-widened exactly.  Each function is a direct transcription of one step; there is
+Precision: every float array is computed in the dtype the inputs are widened
+to (widen_bf16's `dtype`): float64 by default, the reference the GPU tests
+compare against; float32 gives the single-precision instance of the same
+code, which the CPU baseline times.  bf16 inputs arrive as uint16 bit patterns
+and are widened exactly.  Each function is a direct transcription of one step; there is
 no blocking, fusion or reordering beyond what the definition states.
 """
 from __future__ import annotations
@@ -34,10 +37,10 @@ import numpy as np
 
 
 # ---------------------------------------------------------------- inputs
-def widen_bf16(bits) -> np.ndarray:
-    """bf16 bit pattern (uint16) -> float64, exactly."""
+def widen_bf16(bits, dtype=np.float64) -> np.ndarray:
+    """bf16 bit pattern (uint16) -> `dtype` (float64 or float32), exactly."""
     b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
-    return b.view(np.float32).astype(np.float64)
+    return b.view(np.float32).astype(dtype)
 
 
 def silu(v):
@@ -127,10 +130,10 @@ def experts_forward(xp, offsets, w_gate, w_up, w_down):
     R = xp.shape[0]
     F = w_gate.shape[2]
     H = w_down.shape[2]
-    G = np.zeros((R, F))
-    U = np.zeros((R, F))
-    A = np.zeros((R, F))
-    O = np.zeros((R, H))
+    G = np.zeros((R, F), dtype=xp.dtype)
+    U = np.zeros((R, F), dtype=xp.dtype)
+    A = np.zeros((R, F), dtype=xp.dtype)
+    O = np.zeros((R, H), dtype=xp.dtype)
     for e in range(w_gate.shape[0]):
         lo, hi = offsets[e], offsets[e + 1]
         if hi == lo:
@@ -146,7 +149,7 @@ def combine(O, gates, row_of):
     """Y[t] = sum over slots j (in order) of g[t,j] * O[row_of[t,j]]; Y = 0 for
     masked tokens."""
     T, k = row_of.shape
-    Y = np.zeros((T, O.shape[1]))
+    Y = np.zeros((T, O.shape[1]), dtype=O.dtype)
     for j in range(k):
         valid = row_of[:, j] >= 0
         Y[valid] += gates[valid, j:j + 1] * O[row_of[valid, j]]
@@ -154,7 +157,8 @@ def combine(O, gates, row_of):
 
 
 def moe_forward(x, w_r, w_gate, w_up, w_down, k, mask=None):
-    """Whole block forward.  All float arguments float64; mask bool[T] or None."""
+    """Whole block forward.  Float arguments all float64 (or all float32);
+    mask bool[T] or None."""
     E = w_r.shape[1]
     z = router_logits(x, w_r)
     idx = select_topk(z, k, mask)
@@ -174,7 +178,7 @@ def combine_backward(dY, O, gates, row_of):
     """dO[row_of[t,j]] = g[t,j] dY[t];  dg[t,j] = <dY[t], O[row_of[t,j]]>."""
     T, k = row_of.shape
     dO = np.zeros_like(O)
-    dg = np.zeros((T, k))
+    dg = np.zeros((T, k), dtype=O.dtype)
     for j in range(k):
         valid = row_of[:, j] >= 0
         r = row_of[valid, j]
@@ -216,7 +220,7 @@ def router_backward(gates, dg, idx, E):
     dz[t, idx_j] = g_j (dg_j - sum_j' g_j' dg_j'), zero on unselected experts
     and on masked tokens."""
     T, k = idx.shape
-    dz = np.zeros((T, E))
+    dz = np.zeros((T, E), dtype=dg.dtype)
     inner = np.sum(gates * dg, axis=1, keepdims=True)
     dzs = gates * (dg - inner)
     for j in range(k):
@@ -228,7 +232,7 @@ def router_backward(gates, dg, idx, E):
 def unpermute_sum(dxp, row_of, T):
     """sum over slots j of dXp[row_of[t,j]] (zero for masked tokens)."""
     k = row_of.shape[1]
-    out = np.zeros((T, dxp.shape[1]))
+    out = np.zeros((T, dxp.shape[1]), dtype=dxp.dtype)
     for j in range(k):
         valid = row_of[:, j] >= 0
         out[valid] += dxp[row_of[valid, j]]
@@ -337,12 +341,12 @@ def lora_forward(x, w_r, w_gate, w_up, w_down, lora, k, mask=None):
     xp = gather_rows(x, row_token, R)
     F = w_gate.shape[2]
     r = lora["a1"].shape[2]
-    G = np.zeros((R, F))
-    U = np.zeros((R, F))
-    A = np.zeros((R, F))
-    O = np.zeros((R, w_down.shape[2]))
-    P1 = np.zeros((R, r))
-    P2 = np.zeros((R, r))
+    G = np.zeros((R, F), dtype=xp.dtype)
+    U = np.zeros((R, F), dtype=xp.dtype)
+    A = np.zeros((R, F), dtype=xp.dtype)
+    O = np.zeros((R, w_down.shape[2]), dtype=xp.dtype)
+    P1 = np.zeros((R, r), dtype=xp.dtype)
+    P2 = np.zeros((R, r), dtype=xp.dtype)
     for e in range(E):
         lo, hi = offsets[e], offsets[e + 1]
         if hi == lo:
@@ -379,8 +383,8 @@ def lora_backward(x, w_r, w_gate, w_up, w_down, lora, fwd, dY):
     dxp = np.zeros_like(xp)
     grads = {n: np.zeros_like(lora[n]) for n in ("a1", "b1_gate", "b1_up", "a2", "b2")}
     r = lora["a1"].shape[2]
-    Q1 = np.zeros((R, r))
-    Q2 = np.zeros((R, r))
+    Q1 = np.zeros((R, r), dtype=xp.dtype)
+    Q2 = np.zeros((R, r), dtype=xp.dtype)
     dG = np.zeros_like(G)
     dU = np.zeros_like(U)
     for e in range(E):

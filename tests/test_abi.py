@@ -196,3 +196,18 @@ def test_lora_sizes_and_errors():
                           FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == _lib.MOE_ERR_WORKSPACE
     assert L.moe_lora_bwd(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(lo), FAKE, FAKE, FAKE, None,
                           FAKE, FAKE, FAKE, FAKE, FAKE, ws, None) == _lib.MOE_ERR_ARG
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU is present: this test would launch on fake pointers")
+def test_launch_failure_maps_to_moe_err_hip():
+    """A launch the HIP runtime refuses (here: no GPU in the machine) comes
+    back as MOE_ERR_HIP with the runtime's message, after every argument check
+    has passed (valid sizes, non-null 16-byte aligned pointers that are never
+    dereferenced on the host)."""
+    L = _lib.lib()
+    d = D()
+    fake = 1 << 20
+    rc = L.moe_fwd(ctypes.byref(d), fake, fake, fake, fake, fake, None, fake, fake, fake, 1 << 30, None)
+    assert rc == _lib.MOE_ERR_HIP, rc
+    msg = L.moe_last_error().decode()
+    assert msg.startswith("router:") and len(msg) > len("router: ")

@@ -73,3 +73,34 @@ def test_kernel_work_units():
     assert bench.kernel_work("down_wgrad", T, Tv, H, E, F, k, R) == ("flop", 2.0 * H * F * R)
     assert bench.kernel_work("combine", T, Tv, H, E, F, k, R) == ("byte", float(R * H * 2 + Tv * H * 2))
     assert bench.kernel_work("topk", T, Tv, H, E, F, k, R)[0] == "none"
+
+
+def test_cpu_baseline_leg_and_parity_block():
+    """The CPU-baseline leg times the oracle's fp32 instance and reports the
+    affinity cores; its parity block compares GPU-shaped outputs with the fp64
+    oracle (here outputs built from the oracle itself, so every error is 0
+    except for bf16 rounding, and a flipped token is detected and left out)."""
+    import numpy as np
+
+    import bench
+    import workloads
+    from oracle import moe_oracle as O
+    inp = workloads.make("tiny")
+    d = inp["dims"]
+    w = {n: O.widen_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    f = O.moe_forward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], d["k"])
+    b = O.moe_backward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, w["dy"])
+    idx = f["idx"].copy()
+    t_flip = 5
+    idx[t_flip] = [e for e in range(d["E"]) if e not in idx[t_flip]][:d["k"]]
+    gpu = dict(topk_idx=idx, counts=f["counts"], offsets=f["offsets"], row_token=f["row_token"],
+               y=f["Y"], dx=b["dx"], dw_r=b["dw_r"])
+    for n in ("dw_gate", "dw_up", "dw_down"):
+        gpu[n] = (lambda a: (lambda e: a[e]))(b[n])
+    base, par = bench.cpu_baseline(inp, d["k"], d["T"], gpu)
+    assert base["kind"] == "oracle" and base["cores"] >= 1 and base["value"] > 0
+    assert "fp32" in base["sample"]
+    assert par["flipped"] == 1 and not par["counts_offsets_bit_exact"]
+    assert par["experts_compared"] == d["E"] - len(set(idx[t_flip]) | set(f["idx"][t_flip]))
+    assert par["y_max_rel"] == 0 and par["dx_max_rel"] == 0 and par["dw_r_max_rel"] == 0
+    assert par["within_2e-2"]

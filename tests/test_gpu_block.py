@@ -9,8 +9,8 @@ import pytest
 
 import workloads
 from oracle import moe_oracle as O
-from tests.parity import (TOL, assert_close, assert_router_grad, check_permutation_valid,
-                          check_routing, dev_bf16, host, router_grad_bound)
+from tests.parity import (Guards, assert_close, check_permutation_valid, check_routing, dev_bf16, host,
+                          row_pairs, touched_experts)
 
 pytestmark = pytest.mark.gpu
 
@@ -33,6 +33,11 @@ def gpu_run(inp, dw_fp32=False, repeat=1, recompute=False):
           f"mask={mask is not None} dw_fp32={dw_fp32} recompute={recompute}", flush=True)
     blk = moe.MoEBlock(d["T"], d["H"], d["E"], d["F"], d["k"], mask=mask is not None,
                        dw_fp32=dw_fp32, recompute=recompute)
+    # every buffer the library writes sits between sentinel bands
+    guards = Guards()
+    for n in ("saved", "ws", "y", "dx", "dw_r", "dw_gate", "dw_up", "dw_down"):
+        setattr(blk, n, guards.like(getattr(blk, n)))
+    blk.views = moe.moe_saved_views(blk.d, blk.saved)
     t = {n: dev_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
     tm = None if mask is None else torch.from_numpy(mask.astype(np.uint8)).cuda()
     outs = []
@@ -40,6 +45,7 @@ def gpu_run(inp, dw_fp32=False, repeat=1, recompute=False):
         blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], tm)
         blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
         torch.cuda.synchronize()
+        guards.check()
         v = blk.views
         R = int(v["offsets"][-1].item())
         out = {n: host(v[n]) for n in ("logits", "topk_idx", "gates", "counts", "offsets",
@@ -52,38 +58,46 @@ def gpu_run(inp, dw_fp32=False, repeat=1, recompute=False):
     return outs if repeat > 1 else outs[0]
 
 
-def compare(inp, g, f, b):
+def compare(inp, g, f, b, case=None):
+    """Every GPU output against the oracle's.  Without near-tie flips the
+    routing tables are bit-exact and every tensor is compared whole.  A token
+    whose near tie made the GPU pick another expert set is left out of the
+    token-wise comparisons (Y, dX, its rows of Xp, G, U, A, O), and the experts
+    it reaches under either routing are left out of the weight-gradient and
+    dW_r comparisons; everything else is still compared, and the flip is
+    recorded."""
     d = inp["dims"]
     mask = inp["mask"]
+    E = d["E"]
     n_set, n_order, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"],
-                                            g["topk_idx"], g["gates"], d["k"], mask)
-    check_permutation_valid(g["topk_idx"], g["counts"], g["offsets"], g["row_token"], g["row_of"],
-                            d["E"])
-    if flipped.any():
-        pytest.skip(f"{flipped.sum()} near-tie tokens chose a different expert set; "
-                    "choose another seed for an element-wise comparison")
-    if n_order == 0:
-        assert np.array_equal(g["row_of"], f["row_of"])
-    assert np.array_equal(g["counts"], f["counts"])
-    assert np.array_equal(g["offsets"], f["offsets"])
-    assert np.array_equal(g["row_token"], f["row_token"])
-    R = f["R"]
-    # the gather is a byte copy
-    assert np.array_equal(g["xp"], f["xp"])
-    # order ties permute slots (and so row_of columns) but not the rows
-    for n, ref in (("g", f["G"]), ("u", f["U"]), ("a", f["A"]), ("o", f["O"])):
-        if R:
-            assert_close(n, g[n], ref)
-    assert_close("y", g["y"], f["Y"])
-    for n in ("dx", "dw_gate", "dw_up", "dw_down"):
-        assert_close(n, g[n], b[n])
-    bound = router_grad_bound(f, O.widen_bf16(inp["dy"]), O.widen_bf16(inp["x"]))
-    assert_router_grad(g["dw_r"], b["dw_r"], bound)
+                                            g["topk_idx"], g["gates"], d["k"], mask, case=case)
+    check_permutation_valid(g["topk_idx"], g["counts"], g["offsets"], g["row_token"], g["row_of"], E)
+    if not flipped.any():
+        if n_order == 0:
+            assert np.array_equal(g["row_of"], f["row_of"])
+        assert np.array_equal(g["counts"], f["counts"])
+        assert np.array_equal(g["offsets"], f["offsets"])
+        assert np.array_equal(g["row_token"], f["row_token"])
+    keep = ~flipped
+    valid = np.ones(d["T"], dtype=bool) if mask is None else mask.astype(bool)
+    gr, rr = row_pairs(g["topk_idx"], g["row_of"], f["idx"], f["row_of"], np.nonzero(keep & valid)[0])
+    if len(gr):
+        # the gather is a byte copy
+        assert np.array_equal(g["xp"][gr], f["xp"][rr])
+        for n, ref in (("g", f["G"]), ("u", f["U"]), ("a", f["A"]), ("o", f["O"])):
+            if g[n] is not None:
+                assert_close(n, g[n][gr], ref[rr], case=case)
+    assert_close("y", g["y"][keep], f["Y"][keep], case=case)
+    assert_close("dx", g["dx"][keep], b["dx"][keep], case=case)
+    cols = ~touched_experts(flipped, g["topk_idx"], f["idx"], E)
+    for n in ("dw_gate", "dw_up", "dw_down"):
+        assert_close(n, g[n][cols], b[n][cols], case=case)
+    assert_close("dw_r", g["dw_r"][:, cols], b["dw_r"][:, cols], case=case)
     if mask is not None:
-        m = ~mask.astype(bool)
+        m = ~valid
         assert np.all(g["y"][m] == 0) and np.all(g["dx"][m] == 0)
     # experts without rows have exactly zero weight gradients
-    empty = np.nonzero(f["counts"] == 0)[0]
+    empty = np.nonzero(g["counts"] == 0)[0]
     for n in ("dw_gate", "dw_up", "dw_down"):
         assert np.all(g[n][empty] == 0)
 
@@ -92,7 +106,7 @@ def test_tiny_workload_fwd_bwd():
     """T=256, H=128, E=8, top-2, F=256 (the tiny workload), element-wise."""
     inp = workloads.make("tiny")
     f, b = oracle_run(inp)
-    compare(inp, gpu_run(inp), f, b)
+    compare(inp, gpu_run(inp), f, b, case="tiny")
 
 
 def test_tiny_workload_fp32_weight_grads():
@@ -104,15 +118,22 @@ def test_tiny_workload_fp32_weight_grads():
     inp = workloads.make("tiny")
     f, b = oracle_run(inp)
     g = gpu_run(inp, dw_fp32=True)
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["topk_idx"], g["gates"],
+                                  inp["dims"]["k"])
+    assert not flipped.any(), "a near tie flipped an expert set on the fixed tiny seed"
     for n in ("dw_r", "dw_gate", "dw_up", "dw_down"):
-        assert_close(n, g[n], b[n], tol=1e-2)
+        assert_close(n, g[n], b[n], tol=1e-2, case="tiny_fp32_dw")
 
 
 EDGE = {
     # ragged T over several 128-row tiles per expert, deeper K loops
     "ragged_multi_tile": dict(T=1000, H=512, E=8, k=2, F=384, seed=21),
     "ragged_T": dict(T=300, H=256, E=16, k=4, F=128, seed=22),
-    "single_token": dict(T=1, H=128, E=8, k=2, F=128, seed=23),
+    # one token: dW_r is rank one, x dz^T with dz = g1 g2 (dg1 - dg2) (-1, 1),
+    # so its relative error is that of dg1 - dg2.  bf16-stored O bounds each
+    # dg to ~2^-9 relative; the seed is one whose two gate gradients do not
+    # nearly cancel (asserted from the oracle in the test)
+    "single_token": dict(T=1, H=128, E=8, k=2, F=128, seed=24),
     "top1": dict(T=200, H=128, E=8, k=1, F=128, seed=24),
     "k_equals_E": dict(T=130, H=128, E=8, k=8, F=256, seed=25),
     "max_E_max_k": dict(T=100, H=128, E=256, k=32, F=128, seed=26),
@@ -130,7 +151,10 @@ def test_edge_shapes(case):
     f, b = oracle_run(inp)
     if case == "empty_experts":
         assert (f["counts"] == 0).sum() >= 6
-    compare(inp, gpu_run(inp), f, b)
+    if case == "single_token":
+        dg = b["dg"][0]
+        assert abs(dg[0] - dg[1]) >= 0.25 * np.abs(dg).max(), "single-token case must not nearly cancel"
+    compare(inp, gpu_run(inp), f, b, case="edge_" + case)
 
 
 def test_nan_token():
@@ -154,9 +178,9 @@ def test_nan_token():
     f, _ = oracle_run(dict(inp, x=x0))
     o = np.arange(d["T"]) != bad
     _, _, flipped = check_routing(f["z"][o], f["idx"][o], f["gates"][o], g["logits"][o], idx[o],
-                                  g["gates"][o], d["k"])
+                                  g["gates"][o], d["k"], case="nan_token")
     assert np.all(np.isfinite(g["y"][o]))
-    assert_close("y", g["y"][o][~flipped], f["Y"][o][~flipped])
+    assert_close("y", g["y"][o][~flipped], f["Y"][o][~flipped], case="nan_token")
 
 
 def test_underflowing_gates():
@@ -171,7 +195,7 @@ def test_underflowing_gates():
     assert (g["gates"][:, 1] == 0).sum() >= 20, "the case needs gates that underflow"
     for n in ("dx", "dw_r"):
         assert np.all(np.isfinite(g[n]))
-    compare(inp, g, f, b)
+    compare(inp, g, f, b, case="underflowing_gates")
 
 
 @pytest.mark.parametrize("frac", [0.3, 1.0])
@@ -189,7 +213,7 @@ def test_masked_tokens(frac):
             assert np.all(out[n] == 0), n
         assert np.all(out["row_token"] == -1) and np.all(out["topk_idx"] == -1)
         return
-    compare(inp, out, f, b)
+    compare(inp, out, f, b, case=f"masked_{frac}")
 
 
 def test_bitwise_deterministic():
@@ -208,7 +232,7 @@ def test_recompute_is_bit_identical():
     inp["mask"] = (np.arange(777) % 5 != 3).astype(np.uint8)
     f, b = oracle_run(inp)
     a = gpu_run(inp)
-    compare(inp, a, f, b)
+    compare(inp, a, f, b, case="recompute")
     r = gpu_run(inp, recompute=True)
     assert r["g"] is None and r["u"] is None
     for n in a:
@@ -253,9 +277,11 @@ def test_router_losses(case):
     w = {n: O.widen_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
     mb = None if mask is None else mask.astype(bool)
     f = O.moe_forward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], d["k"], mb)
-    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"], d["k"], mb)
-    if flipped.any():
-        pytest.skip("a near tie chose a different expert set")
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"], d["k"], mb,
+                                  case="router_losses_" + case)
+    # the routing counts enter every token's loss gradient, so a flip anywhere
+    # changes dz everywhere: the fixed seeds must route exactly as the oracle
+    assert not flipped.any(), "a near tie flipped an expert set on the fixed seed"
     l_aux, l_z = O.router_aux_loss(f["z"], f["idx"], coefs[0], coefs[1], mb)
     assert abs(g["loss"][0] - l_aux) <= 1e-4 * abs(l_aux), (g["loss"], l_aux)
     assert abs(g["loss"][1] - l_z) <= 1e-4 * abs(l_z), (g["loss"], l_z)
@@ -263,6 +289,5 @@ def test_router_losses(case):
     b0 = O.moe_backward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, w["dy"])
     # the losses' gradient is the larger part of dW_r here
     assert np.abs(b["dw_r"] - b0["dw_r"]).max() > 0.5 * np.abs(b0["dw_r"]).max()
-    assert_close("dx", g["dx"], b["dx"])
-    bound = router_grad_bound(f, w["dy"], w["x"])
-    assert_router_grad(g["dw_r"], b["dw_r"], bound)
+    assert_close("dx", g["dx"], b["dx"], case="router_losses_" + case)
+    assert_close("dw_r", g["dw_r"], b["dw_r"], case="router_losses_" + case)

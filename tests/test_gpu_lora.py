@@ -8,7 +8,7 @@ import pytest
 
 import workloads
 from oracle import moe_oracle as O
-from tests.parity import assert_close, check_routing, dev_bf16, host
+from tests.parity import assert_close, check_routing, dev_bf16, host, touched_experts
 
 pytestmark = pytest.mark.gpu
 
@@ -60,16 +60,20 @@ def oracle(inp, lo_bits, scale, coefs=(0.0, 0.0)):
     return f, b, mask
 
 
-def compare(inp, g, f, b, mask, tol=2e-2):
+def compare(inp, g, f, b, mask, tol=2e-2, case=None):
+    """Y and dX on every token whose expert set matches the oracle's, and the
+    adapter gradients of every expert no near-tie flip reaches (see the block
+    tests); flips are recorded."""
     d = inp["dims"]
-    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"], d["k"], mask)
-    if flipped.any():
-        pytest.skip("a near tie chose a different expert set")
-    assert_close("y", g["y"], f["Y"])
-    assert_close("dx", g["dx"], b["dx"])
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"], d["k"], mask,
+                                  case=case)
+    keep = ~flipped
+    assert_close("y", g["y"][keep], f["Y"][keep], case=case)
+    assert_close("dx", g["dx"][keep], b["dx"][keep], case=case)
+    cols = ~touched_experts(flipped, g["idx"], f["idx"], d["E"])
     empty = np.nonzero(f["counts"] == 0)[0]
     for n in ADAPTERS:
-        assert_close("d" + n, g["d" + n], b["d" + n], tol)
+        assert_close("d" + n, g["d" + n][cols], b["d" + n][cols], tol, case=case)
         assert np.all(g["d" + n][empty] == 0), n
 
 
@@ -88,7 +92,7 @@ def test_lora_matches_oracle(case):
     inp = workloads.block_inputs(**shape)
     lo, scale = lora_inputs(inp, rank, seed=shape["seed"] + 100)
     f, b, mask = oracle(inp, lo, scale)
-    compare(inp, run(inp, rank, lo, scale), f, b, mask)
+    compare(inp, run(inp, rank, lo, scale), f, b, mask, case="lora_" + case)
 
 
 def test_lora_masked_fp32_grads():
@@ -100,7 +104,7 @@ def test_lora_masked_fp32_grads():
     lo, scale = lora_inputs(inp, 16, seed=166)
     f, b, mask = oracle(inp, lo, scale)
     g = run(inp, 16, lo, scale, dw_fp32=True)
-    compare(inp, g, f, b, mask, tol=1e-2)
+    compare(inp, g, f, b, mask, tol=1e-2, case="lora_masked_fp32")
     v = g["da1"].astype(np.float32)
     assert np.any(v.view(np.uint32) & 0xFFFF), "fp32 gradients hold only bf16 values"
 
@@ -122,4 +126,9 @@ def test_lora_with_router_losses():
     lo, scale = lora_inputs(inp, 16, seed=168)
     coefs = (0.5, 0.05)
     f, b, mask = oracle(inp, lo, scale, coefs)
-    compare(inp, run(inp, 16, lo, scale, coefs=coefs), f, b, mask)
+    g = run(inp, 16, lo, scale, coefs=coefs)
+    # the routing counts enter every token's loss gradient: no flip allowed
+    _, _, flipped = check_routing(f["z"], f["idx"], f["gates"], g["logits"], g["idx"], g["gates"],
+                                  inp["dims"]["k"], mask)
+    assert not flipped.any(), "a near tie flipped an expert set on the fixed seed"
+    compare(inp, g, f, b, mask, case="lora_router_losses")

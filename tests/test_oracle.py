@@ -17,6 +17,7 @@ import scipy.special
 
 import workloads
 from oracle import moe_oracle as O
+from tests.parity import touched_experts
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -488,3 +489,40 @@ def test_bf16_encoding_round_trip():
     assert np.all(np.abs(back - v) <= np.abs(v) * 2.0 ** -8)
     # ties go to the even mantissa: 1 + 2^-8 -> 1; 1 + 3*2^-8 -> 1 + 2^-6
     assert back[5] == 1.0 and back[6] == 1.015625
+
+
+def test_fp32_instance_matches_fp64():
+    """The oracle's single-precision instance (inputs widened to float32; the
+    CPU baseline times it) is the same code in fp32: it routes every token
+    away from near ties exactly as the fp64 instance and agrees with it to
+    fp32 rounding on every output and gradient."""
+    inp = workloads.make("tiny")
+    d = inp["dims"]
+    names = ("x", "w_r", "w_gate", "w_up", "w_down", "dy")
+    runs = {}
+    for dt in (np.float64, np.float32):
+        w = {n: O.widen_bf16(inp[n], dt) for n in names}
+        assert all(v.dtype == dt for v in w.values())
+        f = O.moe_forward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], d["k"])
+        b = O.moe_backward(w["x"], w["w_r"], w["w_gate"], w["w_up"], w["w_down"], f, w["dy"])
+        for n in ("Y", "G", "O"):
+            assert f[n].dtype == dt, n
+        for n in ("dx", "dw_r", "dw_gate", "dw_down"):
+            assert b[n].dtype == dt, n
+        runs[dt] = (f, b)
+    (f64, b64), (f32, b32) = runs[np.float64], runs[np.float32]
+    st, ot = O.near_ties(f64["z"], d["k"])
+    clean = ~(st | ot)
+    assert np.array_equal(f32["idx"][clean], f64["idx"][clean])
+    # a set tie may route differently in fp32: such a token, and the experts it
+    # reaches either way, are left out of the comparison
+    flipped = np.array([set(a) != set(b) for a, b in zip(f32["idx"].tolist(), f64["idx"].tolist())])
+    assert not (flipped & ~st).any()
+    keep = ~flipped
+    cols = ~touched_experts(flipped, f32["idx"], f64["idx"], d["E"])
+    assert keep.sum() >= d["T"] - 2 and cols.sum() >= d["E"] - 4
+    assert np.abs(f32["Y"] - f64["Y"])[keep].max() <= 1e-5 * np.abs(f64["Y"]).max()
+    assert np.abs(b32["dx"] - b64["dx"])[keep].max() <= 1e-4 * np.abs(b64["dx"]).max()
+    for n in ("dw_gate", "dw_up", "dw_down"):
+        assert np.abs(b32[n] - b64[n])[cols].max() <= 1e-4 * np.abs(b64[n]).max(), n
+    assert np.abs(b32["dw_r"] - b64["dw_r"])[:, cols].max() <= 1e-4 * np.abs(b64["dw_r"]).max()
