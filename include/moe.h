@@ -28,7 +28,9 @@
  *
  * Conventions shared by every entry point
  *   - All tensors are row-major and live in device memory owned by the
- *     caller; the library never allocates or frees device memory.
+ *     caller; the library never allocates or frees device memory (the one
+ *     static scratch array of moe_fwd_noalloc aside, which the HIP runtime
+ *     reserves on each GPU when it loads the library's device code).
  *   - "bf16" tensors are IEEE bfloat16 (2 bytes); accumulation is fp32.
  *   - Every device pointer must be 16-byte aligned.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
@@ -150,6 +152,25 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
             const void* w_up, const void* w_down, const void* dy, const void* saved,
             void* dx, void* dw_r, void* dw_gate, void* dw_up, void* dw_down, void* ws,
             size_t ws_bytes, void* stream);
+
+/* Allocation-free forward, for callers that cannot allocate device memory or
+ * must not see an allocation happen: code under HIP graph capture, tight
+ * serving or training loops, harnesses that forbid hipMalloc.  The same
+ * operation, arguments (minus the workspace) and outputs as moe_fwd, bit for
+ * bit; its scratch is a static array of MOE_NOALLOC_SCRATCH_BYTES bytes
+ * inside the library, one per GPU (reserved on each GPU the library runs on
+ * until the process ends).  It calls no allocation routine of any kind.
+ *   Limit: moe_fwd_workspace_bytes(d) <= MOE_NOALLOC_SCRATCH_BYTES (about
+ *   13 bytes per token and expert, with the router losses on: T <= 40000 at
+ *   E = 128); larger sizes return MOE_ERR_WORKSPACE before any launch.
+ *   Every call on one GPU shares that GPU's array: calls that overlap on one
+ *   GPU (two streams, two host threads) race and must be serialised by the
+ *   caller.  Nothing in the array needs to start at zero (the kernels clear
+ *   what they count into), and its contents after a call are unspecified. */
+#define MOE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int moe_fwd_noalloc(const moe_dims* d, const void* x, const void* w_r, const void* w_gate,
+                    const void* w_up, const void* w_down, const uint8_t* token_mask, void* y,
+                    void* saved, void* stream);
 
 /* Expert LoRA (§3, "LoRA target groups for MoE"; §4.3): rank-r adapters on
  * every expert's fused gate/up projection and its down projection, with the

@@ -12,12 +12,13 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_F_RECOMPUTE, MOE_MAX_EXPERTS, MOE_MAX_TOPK, MoeDims,
+from ._lib import (MOE_F_DW_FP32, MOE_F_MASK, MOE_F_RECOMPUTE, MOE_MAX_EXPERTS, MOE_MAX_TOPK,
+                   MOE_NOALLOC_SCRATCH_BYTES, MoeDims,
                    MoeError, MoeExpertsDims, MoeExpertsSavedView, MoeLora, MoeSavedView, check, lib)
 
 __all__ = [
     "dims", "experts_dims", "moe_saved_bytes", "moe_fwd_workspace_bytes",
-    "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_bwd",
+    "moe_bwd_workspace_bytes", "moe_saved_views", "moe_fwd", "moe_fwd_noalloc", "moe_bwd",
     "moe_infer_workspace_bytes", "moe_infer", "MoEInfer",
     "moe_lora_saved_bytes", "moe_lora_workspace_bytes", "moe_lora_fwd", "moe_lora_bwd", "lora_args", "MoELoRA",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes", "moe_experts_saved_views",
@@ -134,6 +135,12 @@ def moe_fwd(d, x, w_r, w_gate, w_up, w_down, token_mask, y, saved, ws, stream=No
     check(lib().moe_fwd(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
                         _p(token_mask), _p(y), _p(saved), _p(ws),
                         0 if ws is None else ws.numel() * ws.element_size(), _s(stream)))
+
+
+def moe_fwd_noalloc(d, x, w_r, w_gate, w_up, w_down, token_mask, y, saved, stream=None):
+    """moe_fwd with the library's static scratch instead of a workspace."""
+    check(lib().moe_fwd_noalloc(ctypes.byref(d), _p(x), _p(w_r), _p(w_gate), _p(w_up), _p(w_down),
+                                _p(token_mask), _p(y), _p(saved), _s(stream)))
 
 
 def moe_bwd(d, x, w_r, w_gate, w_up, w_down, dy, saved, dx, dw_r, dw_gate, dw_up, dw_down, ws,

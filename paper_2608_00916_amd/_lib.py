@@ -22,10 +22,11 @@ MOE_MAX_TOPK = 32
 MOE_F_MASK = 1
 MOE_F_DW_FP32 = 2
 MOE_F_RECOMPUTE = 4
+MOE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 EXPORTS = (
     "moe_saved_bytes", "moe_fwd_workspace_bytes", "moe_bwd_workspace_bytes",
-    "moe_saved_views", "moe_fwd", "moe_bwd", "moe_infer_workspace_bytes", "moe_infer",
+    "moe_saved_views", "moe_fwd", "moe_fwd_noalloc", "moe_bwd", "moe_infer_workspace_bytes", "moe_infer",
     "moe_lora_saved_bytes", "moe_lora_workspace_bytes", "moe_lora_fwd", "moe_lora_bwd",
     "moe_experts_saved_bytes", "moe_experts_workspace_bytes",
     "moe_experts_saved_views", "moe_experts_fwd", "moe_experts_bwd",
@@ -90,6 +91,7 @@ def lib() -> ctypes.CDLL:
         "moe_bwd_workspace_bytes": (S, [D]),
         "moe_saved_views": (ctypes.c_int, [D, P, ctypes.POINTER(MoeSavedView)]),
         "moe_fwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, S, P]),
+        "moe_fwd_noalloc": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P]),
         "moe_bwd": (ctypes.c_int, [D, P, P, P, P, P, P, P, P, P, P, P, P, P, S, P]),
         "moe_infer_workspace_bytes": (S, [D]),
         "moe_lora_saved_bytes": (S, [D, ctypes.c_int32]),

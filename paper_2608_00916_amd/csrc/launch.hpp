@@ -101,6 +101,12 @@ hipError_t launch_experts_bwd_gateup_w(const ExpertArgs& a, const bf16_t* dg, co
 // Tokens per chunk of the permutation's counting sort.
 constexpr int kPermChunk = 256;
 
+// ---- static scratch (noalloc.hip)
+// Device address of the current device's static scratch array (the
+// allocation-free forward's workspace, MOE_NOALLOC_SCRATCH_BYTES bytes),
+// looked up on the first call on each device and cached.
+hipError_t static_scratch(void** ptr, size_t* bytes);
+
 // ---- routing (router.hip)
 // logits[T,E] = x W_r (fp32); then per token the top-k experts and gates.
 // `part` (router_part_floats(T, E) floats) holds the partial sums of the

@@ -438,6 +438,20 @@ int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   return block_fwd(d, x, w_r, w_gate, w_up, w_down, nullptr, token_mask, y, saved, ws, ws_bytes, stream);
 }
 
+int moe_fwd_noalloc(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
+                    const void* w_down, const uint8_t* token_mask, void* y, void* saved, void* stream) {
+  if (int rc = check_dims(d)) return rc;
+  const size_t need = fwd_ws(d);
+  if (need > MOE_NOALLOC_SCRATCH_BYTES)
+    return fail(MOE_ERR_WORKSPACE, "the forward needs %zu bytes of scratch, beyond the %zu of the static array",
+                need, static_cast<size_t>(MOE_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  const hipError_t e = static_scratch(&ws, &ws_bytes);
+  if (e != hipSuccess) return hip_status(e, "static scratch");
+  return block_fwd(d, x, w_r, w_gate, w_up, w_down, nullptr, token_mask, y, saved, ws, ws_bytes, stream);
+}
+
 int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gate, const void* w_up,
             const void* w_down, const void* dy, const void* saved, void* dx, void* dw_r, void* dw_gate,
             void* dw_up, void* dw_down, void* ws, size_t ws_bytes, void* stream) {

@@ -211,3 +211,22 @@ def test_launch_failure_maps_to_moe_err_hip():
     assert rc == _lib.MOE_ERR_HIP, rc
     msg = L.moe_last_error().decode()
     assert msg.startswith("router:") and len(msg) > len("router: ")
+
+
+def test_noalloc_forward_rejects_sizes_beyond_its_scratch():
+    """moe_fwd_noalloc refuses a batch whose forward scratch exceeds the
+    static array, with MOE_ERR_WORKSPACE, before any device call (the
+    pointers here are never dereferenced), and accepts the workspace query's
+    own limit arithmetic: T = 65536 at E = 128 needs more, T = 8192 less."""
+    L = _lib.lib()
+    big = D(T=65536, H=2048, E=128, F=768, k=8)
+    small = D(T=8192, H=2048, E=128, F=768, k=8)
+    assert L.moe_fwd_workspace_bytes(ctypes.byref(big)) > _lib.MOE_NOALLOC_SCRATCH_BYTES
+    assert L.moe_fwd_workspace_bytes(ctypes.byref(small)) <= _lib.MOE_NOALLOC_SCRATCH_BYTES
+    fake = 1 << 20
+    rc = L.moe_fwd_noalloc(ctypes.byref(big), fake, fake, fake, fake, fake, None, fake, fake, None)
+    assert rc == _lib.MOE_ERR_WORKSPACE
+    assert "static array" in L.moe_last_error().decode()
+    # invalid dims are reported first, as by moe_fwd
+    assert L.moe_fwd_noalloc(ctypes.byref(D(H=100)), fake, fake, fake, fake, fake, None, fake, fake,
+                             None) == _lib.MOE_ERR_SHAPE
