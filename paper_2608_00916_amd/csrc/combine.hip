@@ -3,6 +3,7 @@
 // vectors (8 bf16 per lane), sums are fp32 in slot order.
 #include "launch.hpp"
 #include "trace.hpp"
+#include "wgrad_plan.hpp"
 
 namespace moe {
 
@@ -78,11 +79,23 @@ __global__ __launch_bounds__(256) void k_combine(const bf16_t* __restrict__ o, c
   }
 }
 
+// The weight gradients' schedule, built by one extra workgroup of the
+// combine backward (independent work that would cost a launch of its own).
+struct PlanArgs {
+  const int32_t* offsets = nullptr;
+  int E = 0, tpe0 = 0, tpe1 = 0;
+  int32_t* plan = nullptr;
+};
+
 // dO[r_j] = g_j dY[t] for every routed slot of token t (bf16).
 template <int KT>
 __global__ __launch_bounds__(256) void k_combine_bwd(const bf16_t* __restrict__ dy, const float* __restrict__ gates,
                                                      const int32_t* __restrict__ row_of, int T, int H, int k,
-                                                     bf16_t* __restrict__ d_o) {
+                                                     bf16_t* __restrict__ d_o, PlanArgs pa) {
+  if (static_cast<int>(blockIdx.x) == cdiv(T, 4)) {  // the plan workgroup
+    build_wgrad_plan(pa.offsets, pa.E, pa.tpe0, pa.tpe1, pa.plan);
+    return;
+  }
   constexpr int kU = row_chunks<KT, 32>();
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -285,10 +298,18 @@ hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* ro
 }
 
 hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_t* row_of, int T, int H, int k,
-                              bf16_t* d_o, hipStream_t s) {
+                              bf16_t* d_o, hipStream_t s, const int32_t* offsets, int E, int F, int32_t* plan) {
+  PlanArgs pa;
+  if (plan != nullptr) {
+    pa.offsets = offsets;
+    pa.E = E;
+    pa.plan = plan;
+    wgrad_tiles_per_expert(H, F, pa.tpe0, pa.tpe1);
+  }
   {
     TraceScope trace_scope(K_COMBINE_BWD, s);
-    MOE_SLOT_DISPATCH(k_combine_bwd, k, dim3(cdiv(T, 4)), s, dy, gates, row_of, T, H, k, d_o);
+    MOE_SLOT_DISPATCH(k_combine_bwd, k, dim3(cdiv(T, 4) + (plan != nullptr ? 1 : 0)), s, dy, gates, row_of, T, H, k,
+                      d_o, pa);
   }
   return hipGetLastError();
 }

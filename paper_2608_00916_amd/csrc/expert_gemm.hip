@@ -10,6 +10,7 @@
 #include "launch.hpp"
 #include "trace.hpp"
 #include "gemm_core.hpp"
+#include "wgrad_plan.hpp"
 
 #include <algorithm>
 #include <mutex>
@@ -169,18 +170,39 @@ __device__ __forceinline__ void store4(void* out, int64_t idx, const f32x4& v) {
     *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out) + idx) = pack4_bf16(v);
 }
 
-// Weight-gradient jobs: expert e, rows [m0, m0+BM), columns [n0, n0+BNS) of
-// each of the NB gradients (M x N each), K = rows of the expert (0 rows:
-// the tile is written as zeros).  Workgroup job i is logical tile
-// xcd_run(i, .) of E x (M/BM) x (N/BNS): each XCD works through whole
-// experts, whose rows (the K of every tile of an expert) then stay in its L2.
+// Weight-gradient schedule.  Every tile of an expert's weight gradient
+// reduces over that expert's rows (K = n_e), so under skewed routing tile
+// lengths differ by an order of magnitude and equal tile counts per XCD are
+// far from equal work.  A plan built on the device from the offsets
+// (k_wgrad_plan, one small launch per backward) orders the experts by
+// descending rows (ties to the lower index) and numbers the tiles expert by
+// expert in that order; XCD x takes the tiles whose cumulative work (K steps
+// plus kTileFixed per tile) starts in [x W / 8, (x + 1) W / 8), W the total,
+// and the workgroups of an XCD take its tiles round-robin, longest first.
+// An expert's tiles stay on one or two XCDs, so its rows are fetched into few
+// L2s.  Each tile is still computed whole by one workgroup: the schedule
+// changes no result.
+// k_wgrad_plan: the plan (wgrad_plan.hpp) as a launch of its own.
+__global__ __launch_bounds__(256) void k_wgrad_plan(const int32_t* __restrict__ offsets, int E, int tpe0, int tpe1,
+                                                    int32_t* __restrict__ plan) {
+  build_wgrad_plan(offsets, E, tpe0, tpe1, plan);
+}
+
+// Job i of this workgroup in weight gradient q (expert e, rows [m0, m0+BM),
+// columns [n0, n0+BNS) of each of its NB M x N gradients): tile
+// first[x] + j + i n of the plan, x this workgroup's XCD, j its index among
+// the XCD's n workgroups.
 template <class C>
-__device__ __forceinline__ bool wgrad_locate(int i, int E, int M, int N, int& e, int& m0, int& n0) {
-  const int nm = M / C::BM, nn = N / C::BNS;
-  const int logical = xcd_run(i, E * nm * nn);
-  if (logical < 0) return false;
-  e = logical / (nm * nn);
-  const int rem = logical - e * nm * nn;
+__device__ __forceinline__ bool wgrad_locate(int i, const int32_t* plan, int q, int E, int M, int N, int& e, int& m0,
+                                             int& n0) {
+  const int nn = N / C::BNS;
+  const int tpe = (M / C::BM) * nn;
+  const int x = static_cast<int>(blockIdx.x) & (kPlanXcds - 1);
+  const int32_t* first = plan + E + q * (kPlanXcds + 1) + x;
+  const int t = uniform_load(first) + static_cast<int>(blockIdx.x >> 3) + i * static_cast<int>(gridDim.x >> 3);
+  if (t >= uniform_load(first + 1)) return false;
+  const int pos = t / tpe, rem = t - pos * tpe;
+  e = uniform_load(plan + pos);
   m0 = (rem / nn) * C::BM;
   n0 = (rem % nn) * C::BNS;
   return true;
@@ -191,12 +213,13 @@ template <class C_, bool F32>
 struct DownWgradJobs : StagedCopyOut<C_, DownWgradJobs<C_, F32>> {
   using C = C_;
   const int32_t* offsets;
+  const int32_t* plan;
   const bf16_t *act, *d_o;
   int E, H, F;
   void* dw_down;
   __device__ bool get(int i, Job<C>& j) const {
     int e, m0, n0;
-    if (!wgrad_locate<C>(i, E, F, H, e, m0, n0)) return false;
+    if (!wgrad_locate<C>(i, plan, 0, E, F, H, e, m0, n0)) return false;
     const int r0 = uniform_load(offsets + e);
     j.a = act + static_cast<int64_t>(r0) * F + m0;
     j.lda = F;
@@ -234,12 +257,13 @@ template <class C_, bool F32>
 struct GateUpWgradJobs : StagedCopyOut<C_, GateUpWgradJobs<C_, F32>> {
   using C = C_;
   const int32_t* offsets;
+  const int32_t* plan;
   const bf16_t *xp, *dg_in, *du_in;
   int E, H, F;
   void *dw_gate, *dw_up;
   __device__ bool get(int i, Job<C>& j) const {
     int e, m0, n0;
-    if (!wgrad_locate<C>(i, E, H, F, e, m0, n0)) return false;
+    if (!wgrad_locate<C>(i, plan, 1, E, H, F, e, m0, n0)) return false;
     const int r0 = uniform_load(offsets + e);
     const int64_t bofs = static_cast<int64_t>(r0) * F + n0;
     j.a = xp + static_cast<int64_t>(r0) * H + m0;
@@ -739,6 +763,9 @@ int persistent_grid(Kernel kernel, int threads, int64_t max_tiles) {
 // Upper bound of the number of 128-row tiles over all experts.
 int max_row_tiles(int rows_cap, int E) { return cdiv(rows_cap, kRowTile) + E; }
 
+int wgrad_plan_ints(int E) { return E + 2 * (kPlanXcds + 1); }
+
+
 // The dgrad of the down product runs 256-column tiles when F allows, else 128.
 int dgate_parts(int F) { return F % 256 == 0 ? F / 256 : F / 128; }
 
@@ -817,14 +844,14 @@ void gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, bf16_
 
 template <class C, bool F32>
 void down_wgrad(const ExpertArgs& a, const bf16_t* d_o, void* dw_down, hipStream_t s) {
-  DownWgradJobs<C, F32> p{{}, a.offsets, a.act, d_o, a.E, a.H, a.F, dw_down};
+  DownWgradJobs<C, F32> p{{}, a.offsets, a.wgrad_plan, a.act, d_o, a.E, a.H, a.F, dw_down};
   run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.F / C::BM) * (a.H / C::BNS), K_DOWN_WGRAD, s);
 }
 
 template <class C, bool F32>
 void gateup_wgrad(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, void* dw_gate, void* dw_up,
                   hipStream_t s) {
-  GateUpWgradJobs<C, F32> p{{}, a.offsets, a.xp, dg, du, a.E, a.H, a.F, dw_gate, dw_up};
+  GateUpWgradJobs<C, F32> p{{}, a.offsets, a.wgrad_plan, a.xp, dg, du, a.E, a.H, a.F, dw_gate, dw_up};
   run_stream<false, false>(p, static_cast<int64_t>(a.E) * (a.H / C::BM) * (a.F / C::BNS), K_GATEUP_WGRAD, s);
 }
 
@@ -842,6 +869,11 @@ void gateup_wgrad_any(const ExpertArgs& a, const bf16_t* dg, const bf16_t* du, v
 }
 
 }  // namespace
+
+void wgrad_tiles_per_expert(int H, int F, int& tpe_down, int& tpe_gu) {
+  tpe_down = H % 256 == 0 ? (F / Wide::BM) * (H / Wide::BNS) : (F / Narrow::BM) * (H / Narrow::BNS);
+  tpe_gu = (H / WideGU::BM) * (F / WideGU::BNS);
+}
 
 hipError_t launch_gateup_fwd(const ExpertArgs& a, hipStream_t s, bool recompute) {
   using C = GateUpFwd;
@@ -895,6 +927,12 @@ hipError_t launch_gateup_dgrad(const ExpertArgs& a, const bf16_t* dg, const bf16
 
 hipError_t launch_experts_bwd_data(const ExpertArgs& a, const bf16_t* d_o, bf16_t* dg, bf16_t* du,
                                    bf16_t* dxp, void* dw_down, bool dw_f32, hipStream_t s) {
+  if (!a.wgrad_plan_built) {
+    int tpe_down = 0, tpe_gu = 0;
+    wgrad_tiles_per_expert(a.H, a.F, tpe_down, tpe_gu);
+    TraceScope trace_scope(K_WGRAD_PLAN, s);
+    hipLaunchKernelGGL(k_wgrad_plan, dim3(1), dim3(256), 0, s, a.offsets, a.E, tpe_down, tpe_gu, a.wgrad_plan);
+  }
   if (a.F % 256 == 0) down_dgrad<Wide>(a, d_o, dg, du, nullptr, s);
   else down_dgrad<Narrow>(a, d_o, dg, du, nullptr, s);
   if (a.H % 256 == 0) down_wgrad_any<Wide>(a, d_o, dw_down, dw_f32, s);

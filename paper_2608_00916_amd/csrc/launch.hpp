@@ -58,10 +58,19 @@ struct ExpertArgs {
   // dgate_part[r][p] = <dA[r], A[r]> over its column block p
   // (dgate_parts(F) blocks; A = silu(G) U in fp32).
   float* dgate_part = nullptr;
+  // Weight gradients only: their schedule, built on the device per backward
+  // (wgrad_plan_ints(E) ints); launch_experts_bwd_data builds it unless an
+  // earlier kernel of the backward already has (wgrad_plan_built).
+  int32_t* wgrad_plan = nullptr;
+  bool wgrad_plan_built = false;
   LoraArgs lora;
 };
 
 int max_row_tiles(int rows_cap, int E);
+// Ints of the weight gradients' schedule (ExpertArgs::wgrad_plan), and the
+// tiles per expert of the down and gate/up weight gradients it schedules.
+int wgrad_plan_ints(int E);
+void wgrad_tiles_per_expert(int H, int F, int& tpe_down, int& tpe_gu);
 // Column blocks of the down product's dgrad (the dgate_part row length).
 int dgate_parts(int F);
 
@@ -144,9 +153,12 @@ hipError_t launch_offsets_from_counts(const int32_t* counts, int E, int rows, in
 // y[t] = sum_j gates[t,j] o[row_of[t,j]] (0 for masked tokens).
 hipError_t launch_combine(const bf16_t* o, const float* gates, const int32_t* row_of, int T, int H,
                           int k, bf16_t* y, hipStream_t s);
-// dO[row_of[t,j]] = g dY[t] for every routed slot.
+// dO[row_of[t,j]] = g dY[t] for every routed slot.  With `plan` non-null,
+// one more workgroup of the same launch also builds the weight gradients'
+// schedule from `offsets` (E experts, tiles per expert of H x F gradients).
 hipError_t launch_combine_bwd(const bf16_t* dy, const float* gates, const int32_t* row_of, int T, int H, int k,
-                              bf16_t* d_o, hipStream_t s);
+                              bf16_t* d_o, hipStream_t s, const int32_t* offsets = nullptr, int E = 0, int F = 0,
+                              int32_t* plan = nullptr);
 // After the down product's dgrad (which leaves part[r][0..nparts), the inner
 // products <dA[r], A[r]> per column block): dg = <dY[t], O[row]> = sum / g,
 // dz per slot (fp32 [T,k]) and dense over E (bf16 [T,E]).  With a non-zero

@@ -157,6 +157,7 @@ struct BwdWs {
   float *dgate, *dz_slot, *dwr_part;
   float* dgate_part;  // <dA, A> per row and column block of the down product's dgrad
   float* dense;  // dz W_r^T (fp32 [T,H]) when the router losses are on
+  int32_t* plan;  // the weight gradients' schedule
   size_t bytes;
 };
 
@@ -174,6 +175,7 @@ BwdWs bwd_layout(const moe_dims* d, void* base) {
   w.w_rt = c.take<bf16_t>(E * H);
   w.dwr_part = c.take<float>(static_cast<size_t>(dwr_splits(d->T)) * H * E);
   w.dense = router_losses(d) ? c.take<float>(T * H) : nullptr;
+  w.plan = c.take<int32_t>(static_cast<size_t>(wgrad_plan_ints(d->E)));
   w.bytes = c.off;
   return w;
 }
@@ -242,6 +244,7 @@ ExpSaved exp_saved_layout(const moe_experts_dims* d, void* base) {
 
 struct ExpWs {
   bf16_t *dg, *du;
+  int32_t* plan;  // the weight gradients' schedule
   size_t bytes;
 };
 
@@ -251,6 +254,7 @@ ExpWs exp_ws_layout(const moe_experts_dims* d, void* base) {
   ExpWs w;
   w.dg = c.take<bf16_t>(R * F);
   w.du = c.take<bf16_t>(R * F);
+  w.plan = c.take<int32_t>(static_cast<size_t>(wgrad_plan_ints(d->E)));
   w.bytes = c.off;
   return w;
 }
@@ -466,11 +470,15 @@ int moe_bwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
   const Saved sv = saved_layout(d, const_cast<void*>(saved));
   const int T = d->T, H = d->H, E = d->E, F = d->F, k = d->top_k;
   const bool f32 = d->flags & MOE_F_DW_FP32;
-  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.gates, sv.row_of, T, H, k, w.d_o, s);
+  // the combine backward's extra workgroup also builds the weight gradients' schedule
+  hipError_t e = launch_combine_bwd(static_cast<const bf16_t*>(dy), sv.gates, sv.row_of, T, H, k, w.d_o, s,
+                                    sv.offsets, E, F, w.plan);
   if (e != hipSuccess) return hip_status(e, "combine bwd");
   ExpertArgs a{T * k, H, E, F, sv.xp, static_cast<const bf16_t*>(w_gate), static_cast<const bf16_t*>(w_up),
                static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start, sv.tile_desc, sv.g, sv.u, sv.a};
   a.dgate_part = w.dgate_part;
+  a.wgrad_plan = w.plan;
+  a.wgrad_plan_built = true;
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   // dXp reuses dO's memory: the down products that read dO are queued first.
   e = launch_experts_bwd_data(a, w.d_o, w.dg, w.du, /*dxp=*/w.d_o, dw_down, f32, s);
@@ -661,6 +669,7 @@ int moe_experts_bwd(const moe_experts_dims* d, const void* xp, const void* w_gat
   ExpertArgs a{d->rows, d->H, d->E, d->F, static_cast<const bf16_t*>(xp), static_cast<const bf16_t*>(w_gate),
                static_cast<const bf16_t*>(w_up), static_cast<const bf16_t*>(w_down), sv.offsets, sv.tile_start,
                sv.tile_desc, sv.g, sv.u, sv.a};
+  a.wgrad_plan = w.plan;
   if (int rc = recompute_gu(d->flags, a, w.dg, w.du, s)) return rc;
   hipError_t e = launch_experts_bwd(a, static_cast<const bf16_t*>(d_o), w.dg, w.du, static_cast<bf16_t*>(dxp),
                                     dw_gate, dw_up, dw_down, (d->flags & MOE_F_DW_FP32) != 0, s);

@@ -36,7 +36,7 @@ const char* const kNames[K_NUM_KERNELS] = {
     "gateup_fwd",    "down_fwd",     "combine",       "combine_bwd",  "down_dgrad_swiglu",
     "down_wgrad",    "gateup_dgrad", "gateup_wgrad",  "dwr_partial",  "dwr_reduce",   "router_dx",
     "offsets_from_counts", "gateup_recompute", "router_loss", "router_dx_dense", "lora_rows", "lora_wgrad",
-    "gate_bwd"};
+    "gate_bwd", "wgrad_plan"};
 
 }  // namespace
 

@@ -31,6 +31,7 @@ enum KernelId {
   K_LORA_ROWS,
   K_LORA_WGRAD,
   K_GATE_BWD,
+  K_WGRAD_PLAN,
   K_NUM_KERNELS
 };
 
