@@ -27,6 +27,13 @@ __device__ __forceinline__ T uniform_load(const T* p) {
   return *(const __attribute__((address_space(4))) T*)(p);
 }
 
+// 16-byte load with the non-temporal cache policy, for data a kernel streams
+// through once.
+__device__ __forceinline__ uint4 load_nt(const void* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+}
+
 // Round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16_t f2bf(float v) {
   __bf16 b = static_cast<__bf16>(v);

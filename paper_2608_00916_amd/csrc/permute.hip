@@ -14,6 +14,10 @@ namespace moe {
 namespace {
 
 constexpr int kChunk = kPermChunk;  // tokens per workgroup (4 waves x 64 lanes)
+#ifndef MOE_PERM_SCAN_CHUNKS
+#define MOE_PERM_SCAN_CHUNKS 128
+#endif
+constexpr int kScanChunks = MOE_PERM_SCAN_CHUNKS;  // chunk count above which the counts are scanned first
 constexpr int kWords = kChunk / 64;
 
 // bits[e][w] bit l  <=>  token chunk*256 + 64 w + l selected expert e.
@@ -54,15 +58,18 @@ __device__ __forceinline__ void write_tiles(int e, int off, int n, int toff, int
   for (int i = 0; i * 128 < n; ++i) tile_desc[toff + i] = make_int2(off + i * 128, e | (min(128, n - i * 128) << 8));
 }
 
-// Per chunk c (one workgroup): from the chunk counts of every chunk, expert
-// e's rows in chunks before c and in all chunks (integer sums in chunk
-// order), the offsets (an exclusive scan over experts), then the chunk's
+// Per chunk c (one workgroup): expert e's rows in chunks before c and in all
+// chunks, the offsets (an exclusive scan over experts), then the chunk's
 // pairs go to row offsets[e] + (rows of e in earlier chunks) + (rank inside
 // the chunk: a popcount of the lower tokens' bits).  Workgroup 0 also writes
-// counts, offsets[E+1], tile_start[E+1] and the tile table.
+// counts, offsets[E+1], tile_start[E+1] and the tile table.  The per-expert
+// sums over chunks come either from the chunk counts themselves (each
+// workgroup adds them up in chunk order: O(chunks) per workgroup, so
+// quadratic in T overall, cheapest while chunks are few) or, with `scanned`,
+// from k_chunk_scan's exclusive prefix per chunk and its totals row.
 __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restrict__ topk_idx, int T, int E,
                                                          int k, const int32_t* __restrict__ chunk_counts,
-                                                         int nchunks, int32_t* __restrict__ counts,
+                                                         int nchunks, bool scanned, int32_t* __restrict__ counts,
                                                          int32_t* __restrict__ offsets,
                                                          int32_t* __restrict__ tile_start,
                                                          int2* __restrict__ tile_desc,
@@ -74,7 +81,10 @@ __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restri
   const int chunk = blockIdx.x;
   const int e = threadIdx.x;
   int before = 0, total = 0;
-  if (e < E) {
+  if (e < E && scanned) {
+    before = chunk_counts[static_cast<int64_t>(chunk) * E + e];
+    total = chunk_counts[static_cast<int64_t>(nchunks) * E + e];
+  } else if (e < E) {
     constexpr int kBatch = 16;  // independent loads in flight per thread
     for (int c0 = 0; c0 < nchunks; c0 += kBatch) {
       int n[kBatch];
@@ -122,6 +132,27 @@ __global__ __launch_bounds__(kChunk) void k_perm_scatter(const int32_t* __restri
     row_token[r] = t;
     row_of[p] = r;
   }
+}
+
+// Per expert e (one workgroup): the exclusive prefix over chunks of its
+// chunk counts, in place (cnt[c][e] becomes the rows of e in chunks before
+// c), and its total in row nchunks.  Thread i takes a contiguous run of
+// chunks; integer sums, so the result is exact in any order.
+__global__ __launch_bounds__(256) void k_chunk_scan(int32_t* __restrict__ cnt, int nchunks, int E) {
+  __shared__ int tmp[256];
+  const int e = blockIdx.x;
+  const int per = cdiv(nchunks, 256);
+  const int c0 = min(nchunks, static_cast<int>(threadIdx.x) * per), c1 = min(nchunks, c0 + per);
+  int sum = 0;
+  for (int c = c0; c < c1; ++c) sum += cnt[static_cast<int64_t>(c) * E + e];
+  int run = block_exclusive_scan(sum, tmp);
+  for (int c = c0; c < c1; ++c) {
+    const int64_t i = static_cast<int64_t>(c) * E + e;
+    const int v = cnt[i];
+    cnt[i] = run;
+    run += v;
+  }
+  if (threadIdx.x == 255) cnt[static_cast<int64_t>(nchunks) * E + e] = run;
 }
 
 // xp[row_of[t,j]] = x[t] for every routed slot (the same rows as
@@ -190,17 +221,23 @@ __global__ __launch_bounds__(256) void k_offsets_from_counts(const int32_t* __re
 
 }  // namespace
 
-int64_t permute_ws_ints(int T, int E) { return static_cast<int64_t>(cdiv(T, kChunk)) * E; }
+// Chunk counts [chunks][E] and a row of per-expert totals.
+int64_t permute_ws_ints(int T, int E) { return static_cast<int64_t>(cdiv(T, kChunk) + 1) * E; }
 
 hipError_t launch_permute(const int32_t* topk_idx, const bf16_t* x, int T, int H, int E, int k,
                           int32_t* counts, int32_t* offsets, int32_t* tile_start, int2* tile_desc,
                           int32_t* row_token, int32_t* row_of, bf16_t* xp, int32_t* ws, hipStream_t s) {
   const int nchunks = cdiv(T, kChunk);
-  const int32_t* chunk_counts = ws;  // written by the router's top-k
+  int32_t* chunk_counts = ws;  // written by the router's top-k
+  // Past kScanChunks chunks, one scan per expert replaces each scatter
+  // workgroup's own pass over every chunk's counts (linear instead of
+  // quadratic in T).
+  const bool scanned = nchunks > kScanChunks;
   {
     TraceScope trace_scope(K_PERM_SCATTER, s);
+    if (scanned) hipLaunchKernelGGL(k_chunk_scan, dim3(E), dim3(256), 0, s, chunk_counts, nchunks, E);
     hipLaunchKernelGGL(k_perm_scatter, dim3(nchunks), dim3(kChunk), 0, s, topk_idx, T, E, k, chunk_counts, nchunks,
-                       counts, offsets, tile_start, tile_desc, row_token, row_of);
+                       scanned, counts, offsets, tile_start, tile_desc, row_token, row_of);
   }
   if (xp == nullptr) return hipGetLastError();
   // a few waves per CU suffice: each token's row is read once and written k times

@@ -142,6 +142,9 @@ EDGE = {
     "k12_H640": dict(T=150, H=640, E=32, k=12, F=128, seed=28),
     # biased router: several experts receive no rows
     "empty_experts": dict(T=257, H=256, E=32, k=3, F=128, seed=27, zipf_s=1.2, n_cold=6),
+    # more than 128 chunks of 256 tokens: the permutation scans the chunk
+    # counts per expert before scattering
+    "scanned_chunks": dict(T=40000, H=128, E=8, k=2, F=128, seed=29),
 }
 
 
