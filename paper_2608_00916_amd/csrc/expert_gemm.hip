@@ -658,6 +658,7 @@ struct DownDgradJobs {
   static constexpr bool kPrefetch = !kLora;
   using Units = RowUnits<C, C::BN>;
   static constexpr bool kStaged = true;
+  static constexpr bool kDrainLate = true;  // its G and U loads go after the step's operand loads
   static constexpr int kDrainCalls = Units::kSlices;
   struct Drain {
     int64_t base;   // element offset of the tile's (0, 0) in G, U, dG and dU

@@ -455,6 +455,18 @@ struct staged_provider : std::false_type {};
 template <class P>
 struct staged_provider<P, std::void_t<decltype(P::kStaged)>> : std::integral_constant<bool, P::kStaged> {};
 
+// A staged provider that declares `static constexpr bool kDrainLate = true`
+// gets its drain call at the end of the step (after the step's operand loads)
+// instead of at its start.  The vector-memory counter completes in order, so
+// a drain that loads from memory (the SwiGLU backward's G and U) delays every
+// operand load issued after it; issued after the step's loads, it delays one
+// step's fewer.  Plain stores lose by the move (the loads of the next step
+// then queue behind them with less time to spare).
+template <class P, class = void>
+struct drain_late : std::false_type {};
+template <class P>
+struct drain_late<P, std::void_t<decltype(P::kDrainLate)>> : std::integral_constant<bool, P::kDrainLate> {};
+
 // LDS bytes gemm_stream needs for provider P.
 template <class P>
 constexpr int stream_lds() {
@@ -701,10 +713,12 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     char* nxt = smem + (1 - S) * C::kStage;
     uint4 af0[C::FM], bf0[C::FN], af1[C::FM], bf1[C::FN];
     // staged output: one drain call in the first step of each pair while
-    // the staged tile lasts, before the step's fragment reads (a fence keeps
-    // it out of the interleave, where every register is taken)
+    // the staged tile lasts, before the step's fragment reads or, kLate,
+    // after its operand loads (a fence keeps it out of the interleave, where
+    // every register is taken)
     constexpr bool kDrain = kStaged && S == 0;
-    if constexpr (kDrain) {
+    constexpr bool kLate = drain_late<P>::value;
+    if constexpr (kDrain && !kLate) {
       if (d_call < kCalls) drain_next();
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -717,6 +731,11 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
     __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
     interleave<kMfma, kReads, 0x100, 0, 0x200>();
     interleave<kMfma, kWrites, 0x200, kLoads, 0x020>();
+    if constexpr (kDrain && kLate) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (d_call < kCalls) drain_next();
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if constexpr (kDrain) d_call = d_call < kCalls ? d_call + 1 : kCalls;
     lds_barrier();
     lnext();
