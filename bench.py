@@ -285,7 +285,8 @@ def lora_step(moe, t, tm, T, H, E, F, k, Tv, rank, steps, warmup):
 
 def ep_share_step(moe, steps, warmup):
     """One expert-parallel rank's share on its own (the ep_share workload: 16
-    local experts, 8192 rows already grouped by expert): moe_experts_fwd +
+    local experts, the 8359 rows a top-8 router sends them from a T=8192
+    batch, already grouped by expert): moe_experts_fwd +
     moe_experts_bwd, timed after the other regions."""
     import torch
     import workloads

@@ -126,7 +126,11 @@ size_t moe_bwd_workspace_bytes(const moe_dims* d);
  * Returns MOE_OK or MOE_ERR_ARG. */
 int moe_saved_views(const moe_dims* d, void* saved, moe_saved_view* view);
 
-/* Forward of the block.
+/* Forward of the block: the top-k router and the expert FFNs of the paper's
+ * MoE layer (§3, Expert-Parallel MoE Training), the forward equations in the
+ * header above, with the routed rows grouped per expert as expert-parallel
+ * dispatch delivers them to an expert's owner (§3, "Expert parallelism and
+ * topology").
  *   x          [T, H]  bf16 tokens
  *   w_r        [H, E]  bf16 router weight
  *   w_gate     [E, H, F], w_up [E, H, F], w_down [E, F, H]  bf16 expert weights
@@ -140,8 +144,9 @@ int moe_fwd(const moe_dims* d, const void* x, const void* w_r, const void* w_gat
             const void* w_up, const void* w_down, const uint8_t* token_mask, void* y,
             void* saved, void* ws, size_t ws_bytes, void* stream);
 
-/* Backward of the block, from the `saved` buffer of the matching moe_fwd
- * (same d, x and weights).
+/* Backward of the block (the training step of §3, Expert-Parallel MoE
+ * Training): the backward equations in the header above, from the `saved`
+ * buffer of the matching moe_fwd (same d, x and weights).
  *   dy      [T, H] bf16 upstream gradient
  *   dx      [T, H] bf16
  *   dw_r    [H, E], dw_gate [E, H, F], dw_up [E, H, F], dw_down [E, F, H]:

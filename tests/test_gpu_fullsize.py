@@ -190,8 +190,9 @@ def test_qwen3_30b_a3b_router_losses_fullsize():
 
 
 def test_ep_share_fullsize():
-    """One expert-parallel rank: 16 local experts, 8192 dispatched rows;
-    every output and gradient compared element-wise."""
+    """One expert-parallel rank: 16 local experts and the 8359 rows a top-8
+    router sends them from a T=8192 batch; every output and gradient compared
+    element-wise."""
     import torch
     import paper_2608_00916_amd as moe
     inp = workloads.make("ep_share")

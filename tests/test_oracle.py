@@ -471,6 +471,29 @@ def test_workload_routing_statistics():
     assert 8.0 < c.max() / c.mean() < 12.0
 
 
+def test_ep_share_rows_are_the_oracle_routing():
+    """The stored rows of the expert-parallel share are what the oracle router
+    sends to experts 0..15 on the seed-2 Qwen-shape batch (re-derived here),
+    and the workload gathers exactly those token rows of that batch."""
+    import importlib.util
+    path = os.path.join(os.path.dirname(__file__), "golden", "make_ep_share_rows.py")
+    spec = importlib.util.spec_from_file_location("make_ep_share_rows", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    counts, row_token = mod.compute()
+    stored_tokens, stored_counts = workloads.ep_rows(8192, 2048, 128, 8, 2, 16)
+    assert list(stored_counts) == counts and list(stored_tokens) == row_token
+    # expert-major, tokens ascending within each expert, each token at most once per expert
+    off = np.concatenate([[0], np.cumsum(counts)])
+    for e in range(16):
+        seg = np.asarray(row_token[off[e]:off[e + 1]])
+        assert np.all(np.diff(seg) > 0)
+    d = workloads.make("ep_share")
+    x = workloads.make("qwen3_30b_a3b", seed=2, only=set())["x"]
+    assert d["dims"]["R"] == sum(counts) == d["xp"].shape[0]
+    assert np.array_equal(d["xp"], x[np.asarray(row_token)])
+
+
 def test_long_passage_mask():
     d = workloads.make("long_passage", only=set())
     m = d["mask"].reshape(16, 4096)

@@ -11,8 +11,9 @@ experts, top-8 routing):
 
 * ``tiny``          T=256,  H=128,  E=8,   k=2, F=256   (seconds on the oracle)
 * ``qwen3_30b_a3b`` T=8192, H=2048, E=128, k=8, F=768   (one GPU, near-uniform router)
-* ``ep_share``      16 local experts, H=2048, F=768, 8192 dispatched rows
-                    (one expert-parallel rank's share of a T=8192, E=128, k=8 routing)
+* ``ep_share``      16 local experts, H=2048, F=768: the rows a T=8192, E=128,
+                    k=8 routing sends to experts 0..15 (one expert-parallel
+                    rank's share; 8359 rows, stored in tests/golden)
 * ``zipf``          T=32768, qwen shape, router biased so that expert
                     popularity follows Zipf(s=1.2); 4 experts get no rows
 * ``long_passage``  T=65536 = 16 passages x 4096 tokens, qwen shape, tokens
@@ -25,6 +26,7 @@ not depend on how many threads generate them.  bf16 values are carried as
 """
 from __future__ import annotations
 
+import json
 import os
 from concurrent.futures import ThreadPoolExecutor
 
@@ -35,7 +37,7 @@ CHUNK = 1 << 22
 CONFIGS = {
     "tiny": dict(kind="block", T=256, H=128, E=8, k=2, F=256, seed=0),
     "qwen3_30b_a3b": dict(kind="block", T=8192, H=2048, E=128, k=8, F=768, seed=1),
-    "ep_share": dict(kind="experts", R=8192, H=2048, E=16, F=768, seed=2,
+    "ep_share": dict(kind="experts", H=2048, E=16, F=768, seed=2,
                      E_total=128, k=8, T=8192),
     "zipf": dict(kind="block", T=32768, H=2048, E=128, k=8, F=768, seed=3,
                  zipf_s=1.2, zipf_scale=0.4, n_cold=4),
@@ -137,16 +139,35 @@ def block_inputs(T, H, E, k, F, seed, zipf_s=None, zipf_scale=0.4, n_cold=0,
                 mask=mask, dims=dict(T=T, H=H, E=E, k=k, F=F))
 
 
-def experts_inputs(R, H, E, F, seed, **_):
-    """Inputs of one expert-parallel rank's share: xp[R,H] rows already grouped
+EP_ROWS = os.path.join(os.path.dirname(os.path.abspath(__file__)), "tests", "golden", "ep_share_rows.json")
+
+
+def ep_rows(T, H, E_total, k, seed, E):
+    """Token index of each row a rank holding experts 0..E-1 receives, and
+    the per-expert counts: the stored routing of the seed-`seed` batch (the
+    file records the batch it was computed on)."""
+    with open(EP_ROWS) as f:
+        doc = json.load(f)
+    src = doc["source"]
+    want = dict(T=T, H=H, E=E_total, k=k, seed=seed, local_experts=E)
+    if any(src[n] != v for n, v in want.items()):
+        raise ValueError(f"{EP_ROWS} holds the routing of {src}, not {want}")
+    return (np.asarray(doc["row_token"], dtype=np.int64),
+            np.asarray(doc["counts"], dtype=np.int32))
+
+
+def experts_inputs(H, E, F, seed, E_total, k, T, **_):
+    """Inputs of one expert-parallel rank's share: xp[R,H] rows grouped
     expert-major, counts[E] (int32, sum R), w_gate/w_up[E,H,F], w_down[E,F,H],
-    d_o[R,H].  Counts are a multinomial draw over near-uniform experts, the
-    statistics a near-uniform top-k router produces."""
+    d_o[R,H].  The rows are the tokens of a T x H batch (drawn as the block
+    workloads draw x, same seed) that a top-k router sends to experts 0..E-1,
+    in expert-major, token-ascending order."""
+    row_token, counts = ep_rows(T, H, E_total, k, seed, E)
+    R = int(counts.sum())
+    x = block_inputs(T=T, H=H, E=E_total, k=k, F=F, seed=seed, only=set())["x"]
     s = _streams(seed, ["xp", "counts", "w_gate", "w_up", "w_down", "d_o"])
-    g = np.random.Generator(np.random.PCG64(s["counts"]))
-    counts = g.multinomial(R, np.full(E, 1.0 / E)).astype(np.int32)
     return dict(
-        xp=normal_bf16(s["xp"], (R, H), 1.0),
+        xp=np.ascontiguousarray(x[row_token]),
         counts=counts,
         w_gate=normal_bf16(s["w_gate"], (E, H, F), WEIGHT_STD),
         w_up=normal_bf16(s["w_up"], (E, H, F), WEIGHT_STD),
