@@ -400,22 +400,29 @@ def time_block(moe, name, steps, warmup, trace, copy_mib=0, keep=False):
     torch.cuda.synchronize()
     print(f"[bench] {name}: warmup {warmup} done", file=sys.stderr, flush=True)
 
-    # Timed region: exactly `steps` steps, bracketed by synchronisations,
-    # without per-kernel events (three events per step give the fwd/bwd split).
+    # Timed region: exactly `steps` steps, bracketed by synchronisations, with
+    # no event inside it (a timing event recorded between launches leaves the
+    # GPU idle for ~5 us while the stream processes it).
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     ev0.record()
     for i in range(steps):
-        step(marks[i])
+        step()
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms = ev0.elapsed_time(ev1) / steps
     print(f"[bench] {name}: timed {steps} steps: {ms:.3f} ms/step (wall {1e3 * wall / steps:.3f})",
           file=sys.stderr, flush=True)
+
+    # Split region: the same steps again with three events per step, for the
+    # forward / backward split and the per-step spread.
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for i in range(steps):
+        step(marks[i])
+    torch.cuda.synchronize()
 
     def pct(v):
         q = np.percentile(np.asarray(v), [10, 50, 90])
