@@ -449,6 +449,13 @@ int moe_fwd_noalloc(const moe_dims* d, const void* x, const void* w_r, const voi
   if (need > MOE_NOALLOC_SCRATCH_BYTES)
     return fail(MOE_ERR_WORKSPACE, "the forward needs %zu bytes of scratch, beyond the %zu of the static array",
                 need, static_cast<size_t>(MOE_NOALLOC_SCRATCH_BYTES));
+  // the caller's pointers are checked before the runtime is asked for the
+  // array's address, so that every argument error comes back with no HIP call
+  if (int rc = check_ptrs({{"x", x}, {"w_r", w_r}, {"w_gate", w_gate}, {"w_up", w_up}, {"w_down", w_down},
+                           {"y", y}, {"saved", saved}}))
+    return rc;
+  if ((d->flags & MOE_F_MASK) && token_mask == nullptr)
+    return fail(MOE_ERR_ARG, "MOE_F_MASK set but token_mask is NULL");
   void* ws = nullptr;
   size_t ws_bytes = 0;
   const hipError_t e = static_scratch(&ws, &ws_bytes);
