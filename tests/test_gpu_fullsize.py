@@ -63,9 +63,10 @@ def run_block(inp, lora=None, coefs=(0.0, 0.0)):
     return out
 
 
-def check_full(name, check_experts, extra_tokens=256, seed=0, lora=None, coefs=(0.0, 0.0)):
+def check_full(name, check_experts, extra_tokens=256, seed=0, lora=None, coefs=(0.0, 0.0), overrides=None):
     case = name + ("" if lora is None else f"_lora_r{lora[0]}") + ("" if coefs == (0.0, 0.0) else "_router_losses")
-    inp = workloads.make(name)
+    case += "".join(f"_{k}{v}" for k, v in (overrides or {}).items())
+    inp = workloads.make(name, **(overrides or {}))
     d = inp["dims"]
     T, E, k = d["T"], d["E"], d["k"]
     mask = None if inp["mask"] is None else inp["mask"].astype(bool)
@@ -187,6 +188,15 @@ def test_qwen3_30b_a3b_router_losses_fullsize():
     dX on sampled tokens, and the dW_r columns of whole experts (their gate
     part from the sample, the losses' dense part from the whole batch)."""
     check_full("qwen3_30b_a3b", pick_qwen, coefs=(0.01, 0.001))
+
+
+def test_rows_beyond_2gib_fullsize():
+    """The Qwen shape at T=131072: 2^20 routed rows, so Xp, O, dO and dXp
+    hold 4 GiB each and every row-indexed byte offset passes 2^31 (they are
+    formed in 64 bits).  Routing for every token; Y, dX, dW_r and the weight
+    gradients of the least-routed expert on the oracle's token sample."""
+    check_full("qwen3_30b_a3b", lambda c: [int(np.argmin(c))], extra_tokens=128,
+               overrides=dict(T=131072, seed=5))
 
 
 def test_ep_share_fullsize():
