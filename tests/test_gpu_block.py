@@ -145,6 +145,9 @@ EDGE = {
     # more than 128 chunks of 256 tokens: the permutation scans the chunk
     # counts per expert before scattering
     "scanned_chunks": dict(T=40000, H=128, E=8, k=2, F=128, seed=29),
+    # twice the Qwen widths: 64-step K loops over H, six 256-column tiles of
+    # F, eight of H, and ragged two-tile experts
+    "wide_H4096_F1536": dict(T=600, H=4096, E=8, k=2, F=1536, seed=30),
 }
 
 

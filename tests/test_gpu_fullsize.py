@@ -199,6 +199,35 @@ def test_rows_beyond_2gib_fullsize():
                overrides=dict(T=131072, seed=5))
 
 
+def test_bitwise_deterministic_fullsize():
+    """Two fwd+bwd calls on the Zipf batch (T=32768: hot experts, empty
+    experts, the device-built weight-gradient schedule, 64 dW_r splits) give
+    the same bits in every output, routing table and gradient."""
+    import torch
+    import paper_2608_00916_amd as moe
+    inp = workloads.make("zipf")
+    d = inp["dims"]
+    print(f"GPU determinism T={d['T']} H={d['H']} E={d['E']} k={d['k']} F={d['F']}", flush=True)
+    t = {n: dev_bf16(inp[n]) for n in ("x", "w_r", "w_gate", "w_up", "w_down", "dy")}
+    blk = moe.MoEBlock(d["T"], d["H"], d["E"], d["F"], d["k"])
+    names = ("y", "dx", "dw_r", "dw_gate", "dw_up", "dw_down")
+    views = ("logits", "topk_idx", "gates", "counts", "offsets", "row_token", "row_of", "xp", "g", "u", "a", "o")
+    runs = []
+    for _ in range(2):
+        blk.forward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"])
+        blk.backward(t["x"], t["w_r"], t["w_gate"], t["w_up"], t["w_down"], t["dy"])
+        torch.cuda.synchronize()
+        R = int(blk.views["offsets"][-1])
+        snap = {n: getattr(blk, n).clone() for n in names}
+        for n in views:
+            v = blk.views[n]
+            snap[n] = (v[:R] if n in ("xp", "g", "u", "a", "o", "row_token") else v).clone()
+        runs.append(snap)
+    for n in runs[0]:  # bytes, so that floats compare bit for bit
+        assert torch.equal(runs[0][n].contiguous().view(torch.uint8), runs[1][n].contiguous().view(torch.uint8)), n
+    record("zipf_two_runs", bitwise_equal=True)
+
+
 def test_ep_share_fullsize():
     """One expert-parallel rank: 16 local experts and the 8359 rows a top-8
     router sends them from a T=8192 batch; every output and gradient compared
