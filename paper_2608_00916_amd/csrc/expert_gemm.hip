@@ -517,6 +517,7 @@ __device__ __forceinline__ uint4 pack8(const float (&f)[8]) {
 // [rows][r]; b1 [E][r][F], MN-contiguous like W_gate).
 template <bool kLora>
 struct GateUpFwdJobs {
+  static constexpr bool kOpaqueSetup = kLora;  // short of registers with the adapter segment
   using C = GateUpFwd;
   const bf16_t *xp, *w_gate, *w_up;
   const int32_t* tile_start;
@@ -615,6 +616,7 @@ __device__ __forceinline__ float row_sum_dpp(float v) {
 // tile).  B(k = h, n = f) = W_down[e][f][h]: K-contiguous rows of W_down.
 template <class C_, bool kLora>
 struct DownDgradJobs {
+  static constexpr bool kOpaqueSetup = kLora;  // short of registers with the adapter segment
   using C = C_;
   const bf16_t *d_o, *w_down;
   const bf16_t *g_in, *u_in;

@@ -467,6 +467,16 @@ struct drain_late : std::false_type {};
 template <class P>
 struct drain_late<P, std::void_t<decltype(P::kDrainLate)>> : std::integral_constant<bool, P::kDrainLate> {};
 
+// A provider that declares `static constexpr bool kOpaqueSetup = true` has
+// its loaders' per-lane offsets recomputed from the thread index at each job.
+// Streams short of registers (the adapter variants, whose jobs carry a second
+// operand segment) otherwise keep them live across the whole stream, spill
+// them, and each reload's wait drains the operand loads in flight.
+template <class P, class = void>
+struct opaque_setup : std::false_type {};
+template <class P>
+struct opaque_setup<P, std::void_t<decltype(P::kOpaqueSetup)>> : std::integral_constant<bool, P::kOpaqueSetup> {};
+
 // LDS bytes gemm_stream needs for provider P.
 template <class P>
 constexpr int stream_lds() {
@@ -606,9 +616,14 @@ __device__ __forceinline__ void gemm_stream(const P& prov, char* smem) {
   auto lsettle = [&]() {  // skip empty jobs, then set the loaders up for lj
     while (lok && lj.K <= 0) lok = prov.get(++li, lj);
     if (lok) {
-      la.setup(lj.a, lj.lda, lj.m_lim, lj.K, tid);
+      // kOpaqueSetup: the thread index made opaque here, so that the
+      // per-lane offsets are recomputed at each job instead of being held
+      // (and spilled) across the whole stream
+      int t = tid;
+      if constexpr (opaque_setup<P>::value) asm volatile("" : "+v"(t));
+      la.setup(lj.a, lj.lda, lj.m_lim, lj.K, t);
 #pragma unroll
-      for (int i = 0; i < C::NB; ++i) lb[i].setup(lj.b[i], lj.ldb, lj.n_lim, lj.K, tid);
+      for (int i = 0; i < C::NB; ++i) lb[i].setup(lj.b[i], lj.ldb, lj.n_lim, lj.K, t);
     } else {
       la.disable();
 #pragma unroll
