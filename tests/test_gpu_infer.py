@@ -69,6 +69,18 @@ def test_infer_qwen3_30b_a3b_fullsize():
     assert np.array_equal(y_inf, y_fwd)
 
 
+@pytest.mark.parametrize("name", ["zipf", "long_passage"])
+def test_infer_fullsize_matches_forward(name):
+    """The Zipf batch (T=32768: hot and empty experts) and the masked
+    long-passage batch (T=65536, 78% valid): bitwise equal to the training
+    forward, padding rows of Y zero."""
+    inp = workloads.make(name)
+    y_inf, y_fwd, _ = run_both(inp)
+    assert np.array_equal(y_inf, y_fwd)
+    if inp["mask"] is not None:
+        assert np.all(y_inf[inp["mask"] == 0] == 0)
+
+
 def test_infer_copies_rows_when_x_exceeds_buffer_range():
     """x of 2 GiB (T = 2^20, H = 1024): past the reach of 32-bit buffer
     offsets, so moe_infer gathers the rows into its workspace instead; still
